@@ -1,0 +1,360 @@
+"""Pins for the CPU oracle: checks against what the paper and mathematics fix.
+
+Each ``pin_*`` takes an ``oracle.oracle.Oracle`` and raises AssertionError on a
+mismatch.  They never compare the oracle with itself or with the HIP path:
+
+* golden cases derived by hand from the definition of the split and product
+  (tests/golden/*.txt);
+* the split against an independent RNE conversion (torch's float->bfloat16
+  cast) and numpy's FP32 subtraction;
+* closed forms: bf16-representable inputs give the plain product; a
+  constructed split x = h + l gives exact(A*B) - S = sum lA*lB; small integers
+  give the exact integer GEMM;
+* a brute-force error bound against the exact rational product on tiny sizes.
+
+The mutation tests run the same pins against oracles with planted mistakes.
+"""
+import os
+from fractions import Fraction
+
+import numpy as np
+import torch
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _bits_f32(x):
+    return np.asarray(x, np.float32).view(np.uint32)
+
+
+def _f32_from_bits(u):
+    return np.asarray(u, np.uint32).view(np.float32)
+
+
+def _bf16_to_f32(h):
+    return (np.asarray(h, np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def torch_rne_bf16(x):
+    """Library RNE conversion FP32 -> bf16 bit patterns (torch CPU cast)."""
+    t = torch.from_numpy(np.ascontiguousarray(x, np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def reference_split(x):
+    """The split's definition evaluated with library primitives.
+
+    hi = RNE_bf16(x) via torch; r = x - hi in numpy FP32; lo = RNE_bf16(r)
+    via torch, or 0 where hi is not finite (the non-finite reading).
+    """
+    x = np.ascontiguousarray(x, np.float32)
+    hi = torch_rne_bf16(x)
+    hf = _bf16_to_f32(hi)
+    fin = np.isfinite(hf)
+    with np.errstate(invalid="ignore", over="ignore"):
+        r = np.where(fin, x - np.where(fin, hf, 0), np.float32(0)).astype(np.float32)
+    lo = torch_rne_bf16(r)
+    lo = np.where(fin, lo, np.uint16(0)).astype(np.uint16)
+    return hi, lo
+
+
+def _check_split_equal(x, hi, lo, hi_ref, lo_ref, what):
+    xn = np.isnan(x)
+    # NaN: only NaN-ness of hi is compared (payloads are not part of the
+    # contract); lo must be +0.
+    h_is_nan = np.isnan(_bf16_to_f32(hi))
+    assert np.array_equal(h_is_nan, xn), "%s: NaN-ness of hi differs" % what
+    assert np.all(lo[xn] == 0), "%s: lo of a NaN input is not +0" % what
+    ok = ~xn
+    bad = np.nonzero((hi[ok] != hi_ref[ok]) | (lo[ok] != lo_ref[ok]))[0]
+    if bad.size:
+        i = np.nonzero(ok)[0][bad[0]]
+        raise AssertionError("%s: split mismatch at x=0x%08x: got (%04x,%04x), expected (%04x,%04x)"
+                             % (what, _bits_f32(x[i]), hi[i], lo[i], hi_ref[i], lo_ref[i]))
+
+
+# --------------------------------------------------------------------------
+# split pins
+# --------------------------------------------------------------------------
+
+def load_split_golden():
+    rows = []
+    with open(os.path.join(GOLDEN, "split_cases.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if line:
+                x, h, l = line.split()
+                rows.append((int(x, 16), int(h, 16), int(l, 16)))
+    return rows
+
+
+def pin_golden_split(orc):
+    rows = load_split_golden()
+    x = _f32_from_bits(np.array([r[0] for r in rows], np.uint32))
+    hi, lo = orc.split(x)
+    for (xb, hb, lb), h, l in zip(rows, hi, lo):
+        assert (int(h), int(l)) == (hb, lb), \
+            "golden split x=0x%08x: got (%04x,%04x), expected (%04x,%04x)" % (xb, h, l, hb, lb)
+
+
+def structured_patterns():
+    """FP32 bit patterns covering every rounding class of the split.
+
+    All 2^16 upper halves combined with lower halves at and around the tie
+    (0x7fff, 0x8000, 0x8001), the extremes (0, 1, 0xffff) and a few others.
+    """
+    upper = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0, 1, 0x1234, 0x7fff, 0x8000, 0x8001, 0xbeef, 0xffff], np.uint32)
+    return (upper[:, None] | lows[None, :]).ravel()
+
+
+def pin_split_vs_library(orc, bits=None):
+    """The oracle split equals the definition evaluated with library RNE."""
+    if bits is None:
+        bits = structured_patterns()
+    x = _f32_from_bits(bits)
+    hi, lo = orc.split(x)
+    hi_ref, lo_ref = reference_split(x)
+    _check_split_equal(x, hi, lo, hi_ref, lo_ref, "split vs library RNE")
+
+
+def check_split_range_exhaustive(orc, start, n):
+    """Exhaustive form of pin_split_vs_library over bit patterns [start, start+n).
+
+    The reference is evaluated with torch CPU ops (multi-threaded) for speed;
+    it is the same definition as ``reference_split``.
+    """
+    hi, lo = orc.split_range(start, n)
+    bits = torch.arange(n, dtype=torch.int64).add_(start).to(torch.int32)
+    x = bits.view(torch.float32)
+    hi_ref = x.to(torch.bfloat16)
+    hf = hi_ref.to(torch.float32)
+    fin = torch.isfinite(hf)
+    r = torch.where(fin, x - torch.where(fin, hf, torch.zeros_like(hf)), torch.zeros_like(x))
+    lo_ref = torch.where(fin, r.to(torch.bfloat16).view(torch.int16),
+                         torch.zeros((), dtype=torch.int16))
+    hi_t = torch.from_numpy(hi.view(np.int16))
+    lo_t = torch.from_numpy(lo.view(np.int16))
+    xn = torch.isnan(x)
+    hn = torch.isnan(hi_t.view(torch.bfloat16))
+    what = "exhaustive split [0x%08x,+%d)" % (start, n)
+    assert torch.equal(hn, xn), "%s: NaN-ness of hi differs" % what
+    assert not torch.any(lo_t[xn] != 0), "%s: lo of a NaN input is not +0" % what
+    bad = (~xn) & ((hi_t != hi_ref.view(torch.int16)) | (lo_t != lo_ref))
+    if torch.any(bad):
+        i = int(torch.nonzero(bad)[0, 0])
+        raise AssertionError("%s: split mismatch at x=0x%08x" % (what, (start + i) & 0xffffffff))
+
+
+def pin_split_properties(orc, seed=0):
+    """Mathematical properties of the split that hold for every finite input.
+
+    * r = x - hi is exact (checked in FP64);
+    * |x - hi - lo| <= 2^-17 |x| for normal-range inputs that do not round to inf;
+    * bf16-representable x gives hi = x and lo = 0.
+    """
+    rng = np.random.default_rng(seed)
+    # log-uniform magnitudes over the normal range, random signs and low bits
+    e = rng.integers(-100, 127, size=200000)
+    m = rng.random(200000) + 1.0
+    x = (np.where(rng.random(200000) < 0.5, -1.0, 1.0) * m * np.exp2(e)).astype(np.float32)
+    x = x[np.isfinite(x) & (np.abs(x) < np.float32(3.3e38))]
+    hi, lo = orc.split(x)
+    hf = _bf16_to_f32(hi).astype(np.float64)
+    lf = _bf16_to_f32(lo).astype(np.float64)
+    x64 = x.astype(np.float64)
+    assert np.all(np.isfinite(hf)), "hi overflowed on an in-range input"
+    r32 = (x - _bf16_to_f32(hi)).astype(np.float64)
+    assert np.array_equal(r32, x64 - hf), "x - hi is not exact in FP32"
+    err = np.abs(x64 - hf - lf)
+    assert np.all(err <= np.ldexp(np.abs(x64), -17)), \
+        "split error exceeds 2^-17|x| (max ratio %g)" % np.max(err / np.abs(x64))
+    # bf16-representable values
+    xb = _bf16_to_f32(hi)
+    hb, lb = orc.split(xb)
+    assert np.array_equal(hb, hi), "split of a bf16 value changed it"
+    assert np.all(lb == 0), "split of a bf16 value has nonzero lo"
+
+
+# --------------------------------------------------------------------------
+# product pins
+# --------------------------------------------------------------------------
+
+def pin_golden_gemm(orc):
+    fields = {}
+    with open(os.path.join(GOLDEN, "gemm_cases.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if line:
+                k, v = line.split(":")
+                fields[k.strip()] = v.split()
+    M, N, K = (int(v) for v in fields["M N K"])
+    A = _f32_from_bits(np.array([int(v, 16) for v in fields["A"]], np.uint32)).reshape(M, K)
+    B = _f32_from_bits(np.array([int(v, 16) for v in fields["B"]], np.uint32)).reshape(K, N)
+    S_exp = sum(Fraction(2) ** int(t) for t in fields["S_terms"])
+    C_exp = np.array([int(v, 16) for v in fields["C"]], np.uint32)
+    C, S = orc.gemm3(A, B)
+    assert Fraction(float(S[0, 0])) == S_exp, "golden GEMM S = %r, expected %r" % (S[0, 0], float(S_exp))
+    assert np.array_equal(_bits_f32(C).ravel(), C_exp), \
+        "golden GEMM C = 0x%08x, expected 0x%08x" % (_bits_f32(C).ravel()[0], C_exp[0])
+
+
+def _short_bf16(shape, rng, emin=-4, emax=3):
+    """bf16-representable values sign * (128..255)/128 * 2^e, e in [emin, emax]."""
+    sig = rng.integers(128, 256, size=shape).astype(np.float64) / 128.0
+    e = rng.integers(emin, emax + 1, size=shape)
+    s = np.where(rng.random(shape) < 0.5, -1.0, 1.0)
+    return (s * sig * np.exp2(e)).astype(np.float32)
+
+
+def pin_bf16_inputs(orc, seed=1, shape=(13, 17, 40)):
+    """bf16-representable A and B: lo = 0 and the result is the plain product.
+
+    With 8-bit significands and exponents in [-4, 3] every partial sum is exact
+    in FP64, so S must equal numpy's FP64 matmul exactly and C its FP32 rounding.
+    """
+    M, N, K = shape
+    rng = np.random.default_rng(seed)
+    A = _short_bf16((M, K), rng)
+    B = _short_bf16((K, N), rng)
+    assert np.all(orc.split(A)[1] == 0) and np.all(orc.split(B)[1] == 0)
+    ref = A.astype(np.float64) @ B.astype(np.float64)
+    C, S = orc.gemm3(A, B)
+    assert np.array_equal(S, ref), "bf16 inputs: S differs from the plain product"
+    assert np.array_equal(C, ref.astype(np.float32)), "bf16 inputs: C is not RNE_fp32(S)"
+
+
+def constructed_operand(shape, rng):
+    """x = h + l with h bf16 and l bf16 whose exponent is 10..16 below h's.
+
+    With h in [2^e, 2^(e+1)), |l| < 2^(e-9), which is below half a bf16 step
+    on either side of h (2^(e-8) above, 2^(e-9) below a power of two), so
+    RNE_bf16(x) = h with no tie; l's lowest bit is at least 2^(e-23), so x is
+    exact in FP32 and x - h = l.  The split therefore returns (h, l) exactly.
+    Returns (x, h, l) as float32 arrays.
+    """
+    h = _short_bf16(shape, rng, -3, 3)
+    eh = np.floor(np.log2(np.abs(h.astype(np.float64))))
+    el = eh - rng.integers(10, 17, size=shape)
+    lsig = rng.integers(128, 256, size=shape).astype(np.float64) / 128.0
+    ls = np.where(rng.random(shape) < 0.5, -1.0, 1.0)
+    l = (ls * lsig * np.exp2(el)).astype(np.float32)
+    x64 = h.astype(np.float64) + l.astype(np.float64)
+    x = x64.astype(np.float32)
+    assert np.array_equal(x.astype(np.float64), x64), "constructed x not exact in FP32"
+    return x, h, l
+
+
+def pin_constructed_split(orc, seed=2, shape=(9, 11, 37)):
+    """Closed form: with x = h + l split exactly, exact(A*B) - S = sum lA*lB."""
+    M, N, K = shape
+    rng = np.random.default_rng(seed)
+    A, hA, lA = constructed_operand((M, K), rng)
+    B, hB, lB = constructed_operand((K, N), rng)
+    ha, la = orc.split(A)
+    assert np.array_equal(_bf16_to_f32(ha), hA) and np.array_equal(_bf16_to_f32(la), lA), \
+        "constructed A did not split into (h, l)"
+    C, S = orc.gemm3(A, B)
+    exact = A.astype(np.float64) @ B.astype(np.float64)
+    lolo = lA.astype(np.float64) @ lB.astype(np.float64)
+    scale = np.abs(A.astype(np.float64)) @ np.abs(B.astype(np.float64))
+    resid = np.abs(exact - S - lolo)
+    assert np.all(resid <= 1e-13 * scale), \
+        "exact - S != sum lA*lB (max rel %g)" % np.max(resid / scale)
+
+
+def pin_integer_exact(orc, seed=3):
+    """Small integers: every product and partial sum is exact, S = integer GEMM.
+
+    Case 1: |a| <= 2^11 (hi and lo are exact integers), |b| <= 2^7 (bf16-exact).
+    Case 2: the roles swapped, so each of the two correction terms is exercised.
+    """
+    rng = np.random.default_rng(seed)
+    for (ba, bb, M, N, K) in ((2048, 128, 19, 23, 32), (128, 2048, 21, 17, 31)):
+        A = rng.integers(-ba, ba + 1, size=(M, K)).astype(np.float32)
+        B = rng.integers(-bb, bb + 1, size=(K, N)).astype(np.float32)
+        ref = A.astype(np.int64) @ B.astype(np.int64)
+        assert np.abs(ref).max() < 2 ** 24
+        C, S = orc.gemm3(A, B)
+        assert np.array_equal(S, ref.astype(np.float64)), "integer GEMM: S != exact"
+        assert np.array_equal(C, ref.astype(np.float32)), "integer GEMM: C != exact"
+
+
+def pin_bruteforce_tiny(orc, seed=4):
+    """Tiny sizes against the exact rational product of the FP32 inputs.
+
+    The split drops lo*lo and lo's rounding residual, so per element
+    |S - exact| <= 2.1 * 2^-16 * (|A||B|)_ij; a dropped cross term or a wrong
+    sign costs about 2^-9 and fails it.
+    """
+    rng = np.random.default_rng(seed)
+    for (M, N, K) in ((1, 1, 1), (2, 3, 5), (4, 4, 8), (3, 7, 6)):
+        A = rng.standard_normal((M, K)).astype(np.float32)
+        B = rng.standard_normal((K, N)).astype(np.float32)
+        C, S = orc.gemm3(A, B)
+        for i in range(M):
+            for j in range(N):
+                ex = sum(Fraction(float(A[i, k])) * Fraction(float(B[k, j])) for k in range(K))
+                mag = sum(abs(Fraction(float(A[i, k])) * Fraction(float(B[k, j])))
+                          for k in range(K))
+                err = abs(Fraction(float(S[i, j])) - ex)
+                assert err <= Fraction(21, 10) * Fraction(1, 2 ** 16) * mag, \
+                    "tiny brute force (%d,%d,%d) element (%d,%d): err %g > bound" % (
+                        M, N, K, i, j, float(err))
+
+
+def pin_alpha(orc, seed=5):
+    """alpha scales the FP64 sum before the FP32 rounding.
+
+    A power of two commutes with rounding, so C(2^-3) = C(1) * 2^-3 exactly;
+    the attention scale 1/sqrt(128) gives one rounding of alpha*S.
+    """
+    rng = np.random.default_rng(seed)
+    A = rng.standard_normal((7, 33)).astype(np.float32)
+    B = rng.standard_normal((33, 9)).astype(np.float32)
+    C1, S1 = orc.gemm3(A, B)
+    C8, S8 = orc.gemm3(A, B, alpha=0.125)
+    assert np.array_equal(S1, S8)
+    assert np.array_equal(C8, C1 * np.float32(0.125)), "alpha = 2^-3 is not an exact scale"
+    a = np.float32(1.0 / np.sqrt(128.0))
+    Ca, _ = orc.gemm3(A, B, alpha=a)
+    ref = float(a) * S1
+    assert np.all(np.abs(Ca.astype(np.float64) - ref) <= np.ldexp(np.abs(ref), -24)), \
+        "alpha*S not correctly rounded"
+
+
+def pin_row_subset(orc, seed=6):
+    """Computing selected rows gives the same rows as the full product."""
+    rng = np.random.default_rng(seed)
+    A = rng.standard_normal((40, 70)).astype(np.float32)
+    B = rng.standard_normal((70, 30)).astype(np.float32)
+    C, S = orc.gemm3(A, B)
+    rows = np.array([39, 0, 17, 17, 5])
+    Cr, Sr = orc.gemm3(A, B, rows=rows)
+    assert np.array_equal(Sr, S[rows]) and np.array_equal(Cr, C[rows]), "row subset differs"
+
+
+def pin_nonfinite_propagation(orc):
+    """Non-finite inputs follow IEEE arithmetic of the three products.
+
+    With lo = 0 for a non-finite hi, an infinite A element meets B's lo part in
+    the hiA*loB product: where that lo is nonzero the output is the signed
+    infinity an FP32 GEMM would give, where it is zero (B exact in bf16)
+    inf*0 makes the output NaN.  NaN inputs give NaN in their row.
+    """
+    A = np.array([[1.0, np.inf], [1.0, np.nan], [2.0, 3.0]], np.float32)
+    b1 = np.float32(1.0 + 2.0 ** -12)           # lo = 2^-12, nonzero
+    B_lo = np.array([[1.0, 1.0], [b1, -b1]], np.float32)
+    C, _ = orc.gemm3(A, B_lo)
+    assert C[0, 0] == np.inf and C[0, 1] == -np.inf
+    assert np.all(np.isnan(C[1]))
+    B_exact = np.array([[1.0, 1.0], [1.0, -1.0]], np.float32)
+    C, _ = orc.gemm3(A, B_exact)
+    assert np.all(np.isnan(C[0])), "inf * (lo = 0) must give NaN"
+    assert np.all(np.isnan(C[1]))
+    assert np.array_equal(C[2], np.array([5.0, -1.0], np.float32))
+
+
+SMALL_PINS = [pin_golden_split, pin_split_vs_library, pin_split_properties, pin_golden_gemm,
+              pin_bf16_inputs, pin_constructed_split, pin_integer_exact, pin_bruteforce_tiny,
+              pin_alpha, pin_row_subset, pin_nonfinite_propagation]

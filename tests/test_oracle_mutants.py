@@ -1,0 +1,58 @@
+"""Planted mistakes in the oracle must each fail at least one pin (no GPU).
+
+Each mutation edits the oracle's C source text, builds it into a temporary
+library and runs the pins against it.  Every mutation stays in bounds.
+"""
+import os
+
+import pytest
+
+import pins
+from oracle import build as obuild
+from oracle.oracle import Oracle
+
+MUTATIONS = [
+    ("drop_hiA_loB", "a_hi * b_hi + a_hi * b_lo + a_lo * b_hi", "a_hi * b_hi + a_lo * b_hi"),
+    ("drop_hiA_hiB", "a_hi * b_hi + a_hi * b_lo + a_lo * b_hi", "a_hi * b_lo + a_lo * b_hi"),
+    ("transposed_B_index", "double b_hi = bhk[j], b_lo = blk[j];",
+     "double b_hi = bh[(j % K) * N + (k % N)], b_lo = bl[(j % K) * N + (k % N)];"),
+    ("drop_loA_hiB", "a_hi * b_hi + a_hi * b_lo + a_lo * b_hi", "a_hi * b_hi + a_hi * b_lo"),
+    ("sign_loA_hiB", "a_hi * b_hi + a_hi * b_lo + a_lo * b_hi", "a_hi * b_hi + a_hi * b_lo - a_lo * b_hi"),
+    ("keep_loA_loB", "a_hi * b_hi + a_hi * b_lo + a_lo * b_hi",
+     "a_hi * b_hi + a_hi * b_lo + a_lo * b_hi + a_lo * b_lo"),
+    ("lo_uses_hi_of_B", "double b_hi = bhk[j], b_lo = blk[j];", "double b_hi = bhk[j], b_lo = bhk[j];"),
+    ("reversed_k_of_A", "double a_hi = ah[k], a_lo = al[k];",
+     "double a_hi = ah[K - 1 - k], a_lo = al[K - 1 - k];"),
+    ("truncate_not_round", "if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u)))", "if (0)"),
+    ("ties_away", "if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u)))", "if (dropped >= 0x8000u)"),
+    ("ties_to_odd", "(dropped == 0x8000u && (kept & 1u))", "(dropped == 0x8000u && !(kept & 1u))"),
+    ("lo_not_zero_nonfinite", "if (isfinite(hf)) {", "if (1) {"),
+    ("lo_is_residual_truncated", "l = oracle_bf16_rne(r);", "l = (uint16_t)(bits_of(r) >> 16);"),
+    ("nan_not_quiet", "return (uint16_t)(((u >> 16) & 0x8000u) | 0x7fc0u);", "return (uint16_t)(u >> 16);"),
+    ("alpha_ignored", "c[j] = (float)((double)alpha * s[j]);", "c[j] = (float)s[j];"),
+    ("alpha_after_round", "c[j] = (float)((double)alpha * s[j]);", "c[j] = alpha * (float)s[j];"),
+    ("row_subset_ignored", "int64_t i = rows ? rows[r] : r;", "int64_t i = r < M ? r : M - 1;"),
+    ("float_accumulator", "s[j] += a_hi * b_hi + a_hi * b_lo + a_lo * b_hi;",
+     "s[j] = (float)(s[j] + (a_hi * b_hi + a_hi * b_lo + a_lo * b_hi));"),
+]
+
+
+@pytest.fixture(scope="module")
+def source():
+    with open(obuild.SOURCE) as f:
+        return f.read()
+
+
+@pytest.mark.parametrize("name,old,new", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_mutant_is_caught(tmp_path, source, name, old, new):
+    assert source.count(old) == 1, "mutation %s no longer applies" % name
+    lib = obuild.build_from_source(source.replace(old, new), str(tmp_path / ("lib_%s.so" % name)),
+                                     werror=False)
+    orc = Oracle(lib)
+    failures = []
+    for pin in pins.SMALL_PINS:
+        try:
+            pin(orc)
+        except AssertionError as e:
+            failures.append((pin.__name__, str(e)[:100]))
+    assert failures, "mutation %s passed every pin" % name
