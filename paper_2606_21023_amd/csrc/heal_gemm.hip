@@ -1,0 +1,412 @@
+// The compensated bf16x3 GEMM kernels for gfx950 (MI355X).
+//
+// HEAL Section 4 (GEMM paragraph and its displayed expansion) recovers the
+// bits a 16-bit cast drops by adding residual products on the 16-bit matrix
+// units, accumulating in FP32.  Here both FP32 operands are split into bf16
+// (hi, lo) and C = hiA*hiB + hiA*loB + loA*hiB.
+//
+// Data path of one workgroup (one BM x BN output tile, batch entry b):
+//   HBM --16-byte loads--> VGPRs --split (v_cvt_pk_bf16_f32)--> LDS planes
+//   {A_hi, A_lo, B_hi, B_lo}, k-contiguous, XOR-swizzled, double-buffered
+//   --ds_read_b128--> MFMA fragments --3x v_mfma_f32_16x16x32_bf16--> FP32
+//   accumulators --> FP32 C (16-byte stores).
+// Each FP32 element is split once per workgroup that stages it.
+//
+// Reduction order (identical in every instance, so results are bitwise equal
+// across runs, instances and M): for each output element, K is walked in
+// 32-deep chunks in ascending order; each chunk adds hiA*hiB, then hiA*loB,
+// then loA*hiB into a single FP32 accumulator; the K tail and out-of-range
+// rows/columns are zero-filled.  No split-K, no atomics.
+//
+// MFMA operand roles: the B fragment is the MFMA's first source (16 rows =
+// 16 output columns n) and the A fragment the second (16 columns = output
+// rows m), so each lane's four accumulators are C[m][n..n+3], four
+// consecutive FP32 of one output row, written with one 16-byte store.
+#include "heal.h"
+#include "heal_device.h"
+#include "heal_internal.h"
+
+namespace heal {
+
+namespace {
+
+constexpr int kChunk = 32;  // K depth of one bf16 MFMA: the unit of the reduction order
+
+template <int BM, int BN, int BK, int WM, int WN, int NT>
+struct Tile {
+    static_assert(BK % kChunk == 0, "stage depth must be whole MFMA chunks");
+    static_assert(BM % WM == 0 && BN % WN == 0 && WM % 16 == 0 && WN % 16 == 0, "wave tiling");
+    static constexpr int WAVES_M = BM / WM;
+    static constexpr int CWAVES = WAVES_M * (BN / WN);  // waves that compute
+    static_assert(CWAVES * 64 <= NT && NT % 64 == 0, "compute waves exceed the workgroup");
+    static constexpr int ROWB = BK * 2;                  // bytes per LDS row of one plane
+    static constexpr int NCH = BK / 8;                   // 16-byte chunks per row
+    static constexpr int RPW = BK >= 64 ? 1 : 64 / BK;   // rows sharing one 128-byte window
+    static constexpr int SWM = (NCH < 8 ? NCH : 8) - 1;  // XOR swizzle mask on the chunk index
+    static constexpr int A_PLANE = BM * ROWB;
+    static constexpr int B_PLANE = BN * ROWB;
+    static constexpr int STAGE = 2 * A_PLANE + 2 * B_PLANE;
+    static constexpr int KQ = BK / 4;                    // 4-element quads per row per stage
+    static constexpr int QA = BM * KQ;                   // A quads per stage
+    static constexpr int QBT = BN * KQ;                  // B quads per stage, B stored N x K
+    static constexpr int BB = KQ * (BN / 4);             // 4x4 blocks per stage, B stored K x N
+    static constexpr int ITA = (QA + NT - 1) / NT;
+    static constexpr int ITBT = (QBT + NT - 1) / NT;
+    static constexpr int ITB = (BB + NT - 1) / NT;
+
+    // byte offset of 4 consecutive k (k = 4*kq) of row `row` in a plane
+    static __device__ __forceinline__ int quad_off(int row, int kq)
+    {
+        return row * ROWB + ((((kq >> 1) ^ ((row / RPW) & SWM))) << 4) + ((kq & 1) << 3);
+    }
+    // byte offset of the 16-byte chunk `c` (8 consecutive k) of row `row`
+    static __device__ __forceinline__ int chunk_off(int row, int c)
+    {
+        return row * ROWB + ((c ^ ((row / RPW) & SWM)) << 4);
+    }
+};
+
+// Elements (r, c .. c+3) of a row-major matrix with nr x nc valid entries,
+// zero outside (edge tiles and the K tail).  VEC: the row is 16-byte aligned
+// and nc % 4 == 0, so a quad is either wholly inside or wholly outside.
+template <bool VEC>
+__device__ __forceinline__ f32x4 load_quad_checked(const float *__restrict__ row_ptr, bool row_ok,
+                                                   int64_t c, int64_t nc)
+{
+    f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (VEC) {
+        if (row_ok && c < nc) v = *reinterpret_cast<const f32x4 *>(row_ptr);
+    } else if (row_ok) {
+        if (c < nc) v.x = row_ptr[0];
+        if (c + 1 < nc) v.y = row_ptr[1];
+        if (c + 2 < nc) v.z = row_ptr[2];
+        if (c + 3 < nc) v.w = row_ptr[3];
+    }
+    return v;
+}
+
+__device__ __forceinline__ void store_pair(char *plane, int off, uint32_t a, uint32_t b)
+{
+    u32x2 v = {a, b};
+    *reinterpret_cast<u32x2 *>(plane + off) = v;
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int NT, bool TRANS_B, bool ALPHA, bool VEC>
+__global__ void __launch_bounds__(NT)
+gemm_bf16x3_kernel(GemmArgs p)
+{
+    using T = Tile<BM, BN, BK, WM, WN, NT>;
+    // Work distribution of the loads (see the load lambdas below).
+    constexpr int A_ROWS_PER_PASS = NT / T::KQ;          // A rows covered by one pass of NT threads
+    constexpr int BT_ROWS_PER_PASS = NT / T::KQ;         // same for B stored N x K
+    constexpr int B_NQ = BN / 4;                         // 4-column groups per B row (B stored K x N)
+    constexpr int B_KQ_PER_PASS = NT / B_NQ;             // 4-row groups covered by one pass
+    static_assert(NT % T::KQ == 0 && NT % B_NQ == 0, "load distribution");
+    static_assert((A_ROWS_PER_PASS / T::RPW) % (T::SWM + 1) == 0 || T::ITA == 1,
+                  "swizzle must repeat across A passes");
+    static_assert((BT_ROWS_PER_PASS / T::RPW) % (T::SWM + 1) == 0 || T::ITBT == 1,
+                  "swizzle must repeat across B passes");
+    static_assert(T::ITB == 1 || ((B_KQ_PER_PASS / 2) % (T::SWM + 1)) == 0,
+                  "swizzle must repeat across B passes");
+    static_assert((16 / T::RPW) % (T::SWM + 1) == 0, "swizzle must repeat every 16 rows");
+
+    __shared__ __attribute__((aligned(16))) char smem[2 * T::STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+
+    // ---- tile coordinates: XCD-aware, grouped along M --------------------
+    // Workgroups are dealt to the 8 XCDs round-robin; renumber so each XCD
+    // owns a contiguous range of tiles, then walk tiles in groups of GM
+    // tile-rows so that concurrently running tiles share A and B panels in
+    // that XCD's L2.
+    const int64_t tiles_m = (p.M + BM - 1) / BM;
+    const int64_t tiles_n = (p.N + BN - 1) / BN;
+    const int64_t nb = (int64_t)gridDim.x;
+    int64_t bid = blockIdx.x;
+    {
+        const int64_t x = bid & 7, i = bid >> 3, q = nb >> 3, r = nb & 7;
+        bid = x * q + (x < r ? x : r) + i;
+    }
+    constexpr int GM = 8;
+    const int64_t group = bid / (GM * tiles_n);
+    const int64_t first_m = group * GM;
+    const int64_t gm = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
+    const int64_t in_group = bid - group * GM * tiles_n;
+    const int64_t m0 = (first_m + in_group % gm) * BM;
+    const int64_t n0 = (in_group / gm) * BN;
+
+    const int64_t M = p.M, N = p.N, K = p.K;
+    const int64_t nk = (K + BK - 1) / BK;
+    const bool interior = VEC && m0 + BM <= M && n0 + BN <= N;
+
+    const int wm = wave % T::WAVES_M;
+    const int wn = wave / T::WAVES_M;
+    const bool computes = T::CWAVES * 64 == NT || wave < T::CWAVES;
+    const int fr = lane & 15;   // fragment row (n for B, m for A) within a 16-block
+    const int fg = lane >> 4;   // fragment k-group: k = 8*fg .. 8*fg+7 of the chunk
+
+    // per-thread load coordinates (fixed for the whole tile)
+    const int a_row = tid / T::KQ;                 // + pass * A_ROWS_PER_PASS
+    const int a_kq = tid % T::KQ;
+    const int b_nq = tid % B_NQ;                   // B stored K x N
+    const int b_kq = tid / B_NQ;                   // + pass * B_KQ_PER_PASS
+    const int a_st = T::quad_off(a_row, a_kq);     // LDS store offsets
+    const int bt_st = a_st;                        // B stored N x K uses the A pattern
+
+    for (int64_t b = blockIdx.y; b < p.batch; b += gridDim.y) {
+        const float *__restrict__ A = p.A + b * p.strideA;
+        const float *__restrict__ B = p.B + b * p.strideB;
+        float *__restrict__ C = p.C + b * p.strideC;
+        const float *__restrict__ pa = A + (m0 + a_row) * p.lda + 4 * a_kq;
+        const float *__restrict__ pb = TRANS_B ? B + (n0 + a_row) * p.ldb + 4 * a_kq
+                                               : B + (int64_t)(4 * b_kq) * p.ldb + n0 + 4 * b_nq;
+
+        f32x4 acc[WN / 16][WM / 16];
+#pragma unroll
+        for (int j = 0; j < WN / 16; ++j)
+#pragma unroll
+            for (int i = 0; i < WM / 16; ++i) acc[j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+        f32x4 ra[T::ITA];
+        f32x4 rb[TRANS_B ? T::ITBT : T::ITB][TRANS_B ? 1 : 4];
+
+        // Full stage of an interior tile: unconditional 16-byte loads.
+        auto load_stage_fast = [&](int64_t k0) {
+#pragma unroll
+            for (int it = 0; it < T::ITA; ++it)
+                if (T::QA % NT == 0 || it * NT + tid < T::QA)
+                    ra[it] = *reinterpret_cast<const f32x4 *>(
+                        pa + (int64_t)(it * A_ROWS_PER_PASS) * p.lda + k0);
+            if (TRANS_B) {
+#pragma unroll
+                for (int it = 0; it < T::ITBT; ++it)
+                    if (T::QBT % NT == 0 || it * NT + tid < T::QBT)
+                        rb[it][0] = *reinterpret_cast<const f32x4 *>(
+                            pb + (int64_t)(it * BT_ROWS_PER_PASS) * p.ldb + k0);
+            } else {
+#pragma unroll
+                for (int it = 0; it < T::ITB; ++it)
+                    if (T::BB % NT == 0 || it * NT + tid < T::BB)
+#pragma unroll
+                        for (int kk = 0; kk < 4; ++kk)
+                            rb[it][kk] = *reinterpret_cast<const f32x4 *>(
+                                pb + (k0 + 4 * it * B_KQ_PER_PASS + kk) * p.ldb);
+            }
+        };
+
+        // Any stage: element-wise bounds checks, zero fill outside.
+        auto load_stage_checked = [&](int64_t k0) {
+#pragma unroll
+            for (int it = 0; it < T::ITA; ++it)
+                if (T::QA % NT == 0 || it * NT + tid < T::QA) {
+                    const int64_t r = it * A_ROWS_PER_PASS;
+                    ra[it] = load_quad_checked<VEC>(pa + r * p.lda + k0, m0 + a_row + r < M,
+                                               k0 + 4 * a_kq, K);
+                }
+            if (TRANS_B) {
+#pragma unroll
+                for (int it = 0; it < T::ITBT; ++it)
+                    if (T::QBT % NT == 0 || it * NT + tid < T::QBT) {
+                        const int64_t r = it * BT_ROWS_PER_PASS;
+                        rb[it][0] = load_quad_checked<VEC>(pb + r * p.ldb + k0, n0 + a_row + r < N,
+                                                      k0 + 4 * a_kq, K);
+                    }
+            } else {
+#pragma unroll
+                for (int it = 0; it < T::ITB; ++it)
+                    if (T::BB % NT == 0 || it * NT + tid < T::BB)
+#pragma unroll
+                        for (int kk = 0; kk < 4; ++kk) {
+                            const int64_t kr = k0 + 4 * (it * B_KQ_PER_PASS + b_kq) + kk;
+                            rb[it][kk] = load_quad_checked<VEC>(
+                                pb + (k0 + 4 * it * B_KQ_PER_PASS + kk) * p.ldb, kr < K,
+                                n0 + 4 * b_nq, N);
+                        }
+            }
+        };
+
+        auto store_stage = [&](int buf) {
+            char *s = smem + buf * T::STAGE;
+            char *a_hi = s, *a_lo = s + T::A_PLANE;
+            char *b_hi = s + 2 * T::A_PLANE, *b_lo = b_hi + T::B_PLANE;
+#pragma unroll
+            for (int it = 0; it < T::ITA; ++it) {
+                if (T::QA % NT == 0 || it * NT + tid < T::QA) {
+                    uint32_t h0, l0, h1, l1;
+                    split2(ra[it].x, ra[it].y, h0, l0);
+                    split2(ra[it].z, ra[it].w, h1, l1);
+                    const int off = a_st + it * A_ROWS_PER_PASS * T::ROWB;
+                    store_pair(a_hi, off, h0, h1);
+                    store_pair(a_lo, off, l0, l1);
+                }
+            }
+            if (TRANS_B) {
+#pragma unroll
+                for (int it = 0; it < T::ITBT; ++it) {
+                    if (T::QBT % NT == 0 || it * NT + tid < T::QBT) {
+                        uint32_t h0, l0, h1, l1;
+                        split2(rb[it][0].x, rb[it][0].y, h0, l0);
+                        split2(rb[it][0].z, rb[it][0].w, h1, l1);
+                        const int off = bt_st + it * BT_ROWS_PER_PASS * T::ROWB;
+                        store_pair(b_hi, off, h0, h1);
+                        store_pair(b_lo, off, l0, l1);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int it = 0; it < T::ITB; ++it) {
+                    if (T::BB % NT == 0 || it * NT + tid < T::BB) {
+                        // register transpose: column nn of the 4x4 block is 4 consecutive k
+#pragma unroll
+                        for (int nn = 0; nn < 4; ++nn) {
+                            uint32_t h0, l0, h1, l1;
+                            split2(rb[it][0][nn], rb[it][1][nn], h0, l0);
+                            split2(rb[it][2][nn], rb[it][3][nn], h1, l1);
+                            const int off = T::quad_off(4 * b_nq + nn, b_kq + it * B_KQ_PER_PASS);
+                            store_pair(b_hi, off, h0, h1);
+                            store_pair(b_lo, off, l0, l1);
+                        }
+                    }
+                }
+            }
+        };
+
+        auto compute_stage = [&](int buf) {
+            const char *s = smem + buf * T::STAGE;
+            const char *a_hi = s, *a_lo = s + T::A_PLANE;
+            const char *b_hi = s + 2 * T::A_PLANE, *b_lo = b_hi + T::B_PLANE;
+#pragma unroll
+            for (int ks = 0; ks < BK / kChunk; ++ks) {
+                const int c = ks * 4 + fg;
+                const int a_off = T::chunk_off(wm * WM + fr, c);
+                const int b_off = T::chunk_off(wn * WN + fr, c);
+                bf16x8 ah[WM / 16], al[WM / 16];
+#pragma unroll
+                for (int i = 0; i < WM / 16; ++i) {
+                    ah[i] = *reinterpret_cast<const bf16x8 *>(a_hi + a_off + i * 16 * T::ROWB);
+                    al[i] = *reinterpret_cast<const bf16x8 *>(a_lo + a_off + i * 16 * T::ROWB);
+                }
+#pragma unroll
+                for (int j = 0; j < WN / 16; ++j) {
+                    const bf16x8 bh = *reinterpret_cast<const bf16x8 *>(b_hi + b_off + j * 16 * T::ROWB);
+                    const bf16x8 bl = *reinterpret_cast<const bf16x8 *>(b_lo + b_off + j * 16 * T::ROWB);
+#pragma unroll
+                    for (int i = 0; i < WM / 16; ++i)
+                        acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh, ah[i], acc[j][i], 0, 0, 0);
+#pragma unroll
+                    for (int i = 0; i < WM / 16; ++i)
+                        acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl, ah[i], acc[j][i], 0, 0, 0);
+#pragma unroll
+                    for (int i = 0; i < WM / 16; ++i)
+                        acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh, al[i], acc[j][i], 0, 0, 0);
+                }
+            }
+        };
+
+        // Main loop, one barrier per stage: while the MFMAs consume stage kt
+        // from one LDS buffer, the loads of stage kt+1 are in flight and are
+        // then split into the other buffer.
+        int64_t kt = 0;
+        if (nk > 0) {
+            if (VEC && interior && BK <= K) load_stage_fast(0);
+            else load_stage_checked(0);
+            store_stage(0);
+            __syncthreads();
+        }
+        if (VEC && interior) {
+            const int64_t nk_full = K / BK;  // stages without a K tail
+            for (; kt + 1 < nk_full; ++kt) {
+                const int buf = (int)(kt & 1);
+                load_stage_fast((kt + 1) * BK);
+                if (computes) compute_stage(buf);
+                store_stage(buf ^ 1);
+                __syncthreads();
+            }
+        }
+        for (; kt < nk; ++kt) {
+            const int buf = (int)(kt & 1);
+            if (kt + 1 < nk) load_stage_checked((kt + 1) * BK);
+            if (computes) compute_stage(buf);
+            if (kt + 1 < nk) store_stage(buf ^ 1);
+            __syncthreads();
+        }
+
+        // ---- epilogue: FP32 accumulators -> FP32 C, no downcast ----------
+        if (computes) {
+#pragma unroll
+            for (int j = 0; j < WN / 16; ++j) {
+#pragma unroll
+                for (int i = 0; i < WM / 16; ++i) {
+                    const int64_t m = m0 + wm * WM + i * 16 + fr;
+                    const int64_t n = n0 + wn * WN + j * 16 + 4 * fg;
+                    f32x4 v = acc[j][i];
+                    if (ALPHA) v = v * p.alpha;
+                    if (m < M && n < N) {
+                        float *cp = C + m * p.ldc + n;
+                        if (VEC && p.vecC && n + 4 <= N) {
+                            *reinterpret_cast<f32x4 *>(cp) = v;
+                        } else {
+                            cp[0] = v.x;
+                            if (n + 1 < N) cp[1] = v.y;
+                            if (n + 2 < N) cp[2] = v.z;
+                            if (n + 3 < N) cp[3] = v.w;
+                        }
+                    }
+                }
+            }
+        }
+        if (b + gridDim.y < p.batch) __syncthreads();  // LDS reuse by the next batch entry
+    }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int NT, bool TRANS_B, bool ALPHA>
+hipError_t launch_tile3(const GemmArgs &a, dim3 grid, hipStream_t stream)
+{
+    // The 16-byte path needs every A row and every op(B) row 16-byte aligned
+    // and whole quads along K (A, B stored N x K) or N (B stored K x N).
+    const bool vec = a.vecA && a.vecB && a.K % 4 == 0 && (TRANS_B || a.N % 4 == 0);
+    if (vec)
+        hipLaunchKernelGGL((gemm_bf16x3_kernel<BM, BN, BK, WM, WN, NT, TRANS_B, ALPHA, true>), grid,
+                           dim3(NT), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm_bf16x3_kernel<BM, BN, BK, WM, WN, NT, TRANS_B, ALPHA, false>), grid,
+                           dim3(NT), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int NT>
+hipError_t launch_tile(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
+{
+    const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+    if (tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
+    const dim3 grid((unsigned)tiles, gy);
+    if (trans_b)
+        return use_alpha ? launch_tile3<BM, BN, BK, WM, WN, NT, true, true>(a, grid, stream)
+                         : launch_tile3<BM, BN, BK, WM, WN, NT, true, false>(a, grid, stream);
+    return use_alpha ? launch_tile3<BM, BN, BK, WM, WN, NT, false, true>(a, grid, stream)
+                     : launch_tile3<BM, BN, BK, WM, WN, NT, false, false>(a, grid, stream);
+}
+
+}  // namespace
+
+hipError_t launch_gemm(int instance, const GemmArgs &a, bool trans_b, bool use_alpha,
+                       hipStream_t stream)
+{
+    switch (instance) {
+    case HEAL_INSTANCE_LARGE:
+        return launch_tile<256, 256, 32, 64, 128, 512>(a, trans_b, use_alpha, stream);
+    case HEAL_INSTANCE_MEDIUM:
+        return launch_tile<128, 128, 32, 64, 64, 256>(a, trans_b, use_alpha, stream);
+    case HEAL_INSTANCE_SKINNY:
+        if (a.M <= 16) return launch_tile<16, 64, 64, 16, 16, 256>(a, trans_b, use_alpha, stream);
+        if (a.M <= 32) return launch_tile<32, 64, 64, 32, 16, 256>(a, trans_b, use_alpha, stream);
+        return launch_tile<64, 64, 64, 64, 16, 256>(a, trans_b, use_alpha, stream);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace heal

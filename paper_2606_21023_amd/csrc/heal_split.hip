@@ -1,0 +1,69 @@
+// heal_split_f32: the standalone elementwise split, FP32 -> planar bf16 (hi, lo).
+// HBM-bound: 4 bytes read and 4 bytes written per element.
+#include "heal_device.h"
+#include "heal_internal.h"
+
+namespace heal {
+
+namespace {
+
+constexpr int kSplitThreads = 256;
+
+// VEC: x, hi and lo are 16-byte aligned, so each thread moves 8 elements with
+// two 16-byte loads and two 16-byte stores per step.
+template <bool VEC>
+__global__ void __launch_bounds__(kSplitThreads)
+split_kernel(const float *__restrict__ x, uint16_t *__restrict__ hi, uint16_t *__restrict__ lo,
+             int64_t n)
+{
+    const int64_t stride = (int64_t)gridDim.x * kSplitThreads;
+    const int64_t t = (int64_t)blockIdx.x * kSplitThreads + threadIdx.x;
+    int64_t done = 0;
+    if (VEC) {
+        const int64_t n8 = n / 8;
+        const f32x4 *x4 = reinterpret_cast<const f32x4 *>(x);
+        u32x4 *h4 = reinterpret_cast<u32x4 *>(hi);
+        u32x4 *l4 = reinterpret_cast<u32x4 *>(lo);
+        for (int64_t i = t; i < n8; i += stride) {
+            const f32x4 a = __builtin_nontemporal_load(x4 + 2 * i);
+            const f32x4 b = __builtin_nontemporal_load(x4 + 2 * i + 1);
+            uint32_t h0, h1, h2, h3, l0, l1, l2, l3;
+            split2(a.x, a.y, h0, l0);
+            split2(a.z, a.w, h1, l1);
+            split2(b.x, b.y, h2, l2);
+            split2(b.z, b.w, h3, l3);
+            const u32x4 h = {h0, h1, h2, h3}, l = {l0, l1, l2, l3};
+            __builtin_nontemporal_store(h, h4 + i);
+            __builtin_nontemporal_store(l, l4 + i);
+        }
+        done = n8 * 8;
+    }
+    for (int64_t i = done + t; i < n; i += stride) {
+        uint32_t h, l;
+        split2(x[i], 0.0f, h, l);
+        hi[i] = (uint16_t)h;
+        lo[i] = (uint16_t)l;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_split(const float *x, uint16_t *hi, uint16_t *lo, int64_t n, hipStream_t stream)
+{
+    const bool vec = ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(hi) |
+                       reinterpret_cast<uintptr_t>(lo)) & 15u) == 0;
+    const int64_t per_block = (int64_t)kSplitThreads * (vec ? 8 : 1);
+    int64_t blocks = (n + per_block - 1) / per_block;
+    // enough resident workgroups to saturate HBM on 256 CUs; the loop strides
+    if (blocks > 256 * 16) blocks = 256 * 16;
+    if (blocks < 1) blocks = 1;
+    if (vec)
+        hipLaunchKernelGGL(split_kernel<true>, dim3((unsigned)blocks), dim3(kSplitThreads), 0,
+                           stream, x, hi, lo, n);
+    else
+        hipLaunchKernelGGL(split_kernel<false>, dim3((unsigned)blocks), dim3(kSplitThreads), 0,
+                           stream, x, hi, lo, n);
+    return hipGetLastError();
+}
+
+}  // namespace heal

@@ -1,0 +1,118 @@
+"""The C-ABI library: loads, exports what include/heal.h declares, and rejects
+bad arguments before touching the device (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_21023_amd as heal
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "heal.h")
+
+INVALID = 1
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(heal_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("heal_split_f32", "heal_gemm_f32", "heal_gemm_f32_strided_batched",
+                     "heal_status_string"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = heal.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), "libheal.so does not export %s" % name
+
+
+def test_status_strings_and_version():
+    L = heal.lib()
+    for code, name in heal.STATUS.items():
+        assert L.heal_status_string(code).decode() == name
+    assert L.heal_status_string(99).decode() == "HEAL_ERR_UNKNOWN"
+    assert L.heal_version() >= 100
+
+
+def test_select_instance_depends_on_m_and_n_only():
+    assert heal.select_instance(1, 4096) == heal.INSTANCE_SKINNY
+    assert heal.select_instance(64, 128256) == heal.INSTANCE_SKINNY
+    assert heal.select_instance(65, 4096) in (heal.INSTANCE_MEDIUM, heal.INSTANCE_LARGE)
+    assert heal.select_instance(8192, 8192) == heal.INSTANCE_LARGE
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+@pytest.mark.parametrize("args", [
+    # M, N, K, A, B, C, lda, ldb, ldc
+    (-1, 4, 4, FAKE, FAKE, FAKE, 4, 4, 4),       # negative M
+    (4, -1, 4, FAKE, FAKE, FAKE, 4, 4, 4),       # negative N
+    (4, 4, -1, FAKE, FAKE, FAKE, 4, 4, 4),       # negative K
+    (4, 4, 8, FAKE, FAKE, FAKE, 7, 4, 4),        # lda < K
+    (4, 8, 4, FAKE, FAKE, FAKE, 4, 7, 8),        # ldb < N
+    (4, 8, 4, FAKE, FAKE, FAKE, 4, 8, 7),        # ldc < N
+    (4, 4, 4, 0, FAKE, FAKE, 4, 4, 4),           # null A
+    (4, 4, 4, FAKE, 0, FAKE, 4, 4, 4),           # null B
+    (4, 4, 4, FAKE, FAKE, 0, 4, 4, 4),           # null C
+    (4, 4, 4, FAKE + 2, FAKE, FAKE, 4, 4, 4),    # A not 4-byte aligned
+    (4, 4, 4, FAKE, FAKE, FAKE + 1, 4, 4, 4),    # C not 4-byte aligned
+])
+def test_gemm_rejects_invalid_arguments(args):
+    st = heal.lib().heal_gemm_f32(*args, None)
+    assert st == INVALID
+
+
+def test_empty_products_are_noops_without_device():
+    L = heal.lib()
+    assert L.heal_gemm_f32(0, 4, 4, 0, 0, 0, 4, 4, 4, None) == 0
+    assert L.heal_gemm_f32(4, 0, 4, 0, 0, 0, 4, 1, 1, None) == 0
+    assert L.heal_split_f32(0, 0, 0, 0, None) == 0
+    f = L.heal_gemm_f32_strided_batched
+    assert f(4, 4, 4, ctypes.c_float(1.0), 0, 4, 0, 0, 4, 0, 0, 0, 4, 0, 0, None) == 0  # batch 0
+
+
+@pytest.mark.parametrize("bad", ["trans", "stride", "batch", "ldb_t"])
+def test_batched_rejects_invalid_arguments(bad):
+    f = heal.lib().heal_gemm_f32_strided_batched
+    a = dict(M=4, N=8, K=16, alpha=ctypes.c_float(1.0), A=FAKE, lda=16, sA=64, B=FAKE, ldb=8,
+             sB=128, tb=0, C=FAKE, ldc=8, sC=32, batch=2)
+    if bad == "trans":
+        a["tb"] = 2
+    elif bad == "stride":
+        a["sA"] = -1
+    elif bad == "batch":
+        a["batch"] = -3
+    elif bad == "ldb_t":
+        a["tb"] = 1
+        a["ldb"] = 15   # B stored N x K needs ldb >= K
+    st = f(a["M"], a["N"], a["K"], a["alpha"], a["A"], a["lda"], a["sA"], a["B"], a["ldb"],
+           a["sB"], a["tb"], a["C"], a["ldc"], a["sC"], a["batch"], None)
+    assert st == INVALID
+
+
+def test_split_rejects_invalid_arguments():
+    L = heal.lib()
+    assert L.heal_split_f32(FAKE, FAKE, FAKE, -1, None) == INVALID
+    assert L.heal_split_f32(0, FAKE, FAKE, 8, None) == INVALID
+    assert L.heal_split_f32(FAKE, FAKE + 1, FAKE, 8, None) == INVALID
+
+
+def test_forced_instance_out_of_range_rejected():
+    f = heal.lib().heal_gemm_f32_instance
+    st = f(17, 4, 4, 4, ctypes.c_float(1.0), FAKE, 4, 0, FAKE, 4, 0, 0, FAKE, 4, 0, 1, None)
+    assert st == INVALID
+
+
+def test_binding_fails_loudly_without_library(monkeypatch):
+    monkeypatch.setattr(heal, "_lib", None)
+    monkeypatch.setattr(heal, "library_path", "/nonexistent/libheal.so")
+    with pytest.raises(heal.HealError):
+        heal.lib()

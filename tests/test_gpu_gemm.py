@@ -1,0 +1,282 @@
+"""heal_gemm_f32 on the GPU against the CPU oracle, and its bitwise invariants.
+
+Parity: element by element against the oracle's FP64 sum on the same seeded
+inputs (tolerance bars in gpu_util), exact equality where every partial sum
+is an integer below 2^24.  Invariants (GPU against itself): 10 repeated runs,
+every M for the same row, every kernel instance, plain vs batched entry points.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_21023_amd as heal
+from paper_2606_21023_amd import workloads as wl
+from gpu_util import abs_product, announce, check_tolerance, needs_gpu, to_dev
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+INSTANCES = [heal.INSTANCE_LARGE, heal.INSTANCE_MEDIUM, heal.INSTANCE_SKINNY]
+INAME = {heal.INSTANCE_LARGE: "large", heal.INSTANCE_MEDIUM: "medium",
+         heal.INSTANCE_SKINNY: "skinny"}
+
+
+def gpu_gemm(A, B, instance=None, alpha=1.0, trans_b=False):
+    """Run on numpy inputs; B is K x N (or N x K when trans_b); returns numpy C."""
+    Ad, Bd = to_dev(A), to_dev(B)
+    if instance is None and alpha == 1.0 and not trans_b:
+        C = heal.heal_gemm_f32(Ad, Bd)
+    else:
+        C = heal.heal_gemm_f32_instance(instance or heal.INSTANCE_AUTO, Ad, Bd, alpha=alpha,
+                                        trans_b=trans_b)
+    torch.cuda.synchronize()
+    return C.cpu().numpy()
+
+
+# ---------------------------------------------------------------------------
+# exactness: integer inputs, any summation order gives the exact result
+# ---------------------------------------------------------------------------
+INT_SHAPES = [(1, 1, 1), (17, 33, 31), (300, 257, 32), (65, 129, 17), (16, 64, 32), (513, 70, 5)]
+
+
+@pytest.mark.parametrize("instance", INSTANCES, ids=lambda i: INAME[i])
+@pytest.mark.parametrize("shape", INT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_integer_exact(orc, instance, shape):
+    M, N, K = shape
+    for (ba, bb, seed) in ((2048, 128, 10), (128, 2048, 11)):
+        A = wl.integer_matrix((M, K), seed, ba)
+        B = wl.integer_matrix((K, N), seed + 100, bb)
+        announce("integer exact %s %s bounds %d/%d" % (INAME[instance], shape, ba, bb))
+        C = gpu_gemm(A, B, instance)
+        exact = (A.astype(np.int64) @ B.astype(np.int64)).astype(np.float32)
+        Co, _ = orc.gemm3(A, B)
+        assert np.array_equal(Co, exact)
+        assert np.array_equal(C, exact), "GPU differs from the exact integer GEMM"
+
+
+# ---------------------------------------------------------------------------
+# tolerance parity on small shapes spanning several tiles and ragged tails
+# ---------------------------------------------------------------------------
+SHAPES = [(1, 1, 1), (15, 16, 17), (16, 16, 32), (17, 31, 33), (31, 33, 255), (255, 257, 257),
+          (257, 255, 129), (64, 300, 1000), (300, 64, 64), (129, 513, 96), (33, 1000, 70),
+          (520, 530, 300)]
+
+
+@pytest.mark.parametrize("instance", INSTANCES, ids=lambda i: INAME[i])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_parity_small(orc, instance, shape):
+    M, N, K = shape
+    A = wl.random_matrix((M, K), seed=M * 7 + K)
+    B = wl.random_matrix((K, N), seed=N * 13 + K)
+    announce("parity %s %s" % (INAME[instance], shape))
+    C = gpu_gemm(A, B, instance)
+    _, S = orc.gemm3(A, B)
+    check_tolerance(C, S, abs_product(A, B), "%s %s" % (INAME[instance], shape))
+
+
+@pytest.mark.parametrize("instance", INSTANCES, ids=lambda i: INAME[i])
+@pytest.mark.parametrize("shape", [(17, 31, 33), (255, 257, 257), (64, 300, 1000)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_parity_trans_b_alpha(orc, instance, shape):
+    M, N, K = shape
+    A = wl.random_matrix((M, K), seed=1 + M)
+    Bt = wl.random_matrix((N, K), seed=2 + N)      # stored N x K
+    alpha = float(wl.ATTN_SCALE)
+    announce("parity trans_b alpha %s %s" % (INAME[instance], shape))
+    C = gpu_gemm(A, Bt, instance, alpha=alpha, trans_b=True)
+    B = np.ascontiguousarray(Bt.T)
+    Co, S = orc.gemm3(A, B, alpha=alpha)
+    check_tolerance(C, float(np.float32(alpha)) * S, float(np.float32(alpha)) * abs_product(A, B),
+                    "trans_b alpha %s" % (shape,))
+
+
+@pytest.mark.parametrize("instance", INSTANCES, ids=lambda i: INAME[i])
+def test_parity_padded_and_misaligned(orc, instance):
+    """Leading dimensions above the width and base pointers off 16 bytes."""
+    M, N, K = 70, 90, 77
+    lda, ldb, ldc = K + 5, N + 3, N + 7
+    rng = np.random.default_rng(5)
+    Abuf = rng.standard_normal(M * lda + 1).astype(np.float32)
+    Bbuf = rng.standard_normal(K * ldb + 1).astype(np.float32)
+    A = Abuf[1:].reshape(M, lda)[:, :K]
+    B = Bbuf[1:].reshape(K, ldb)[:, :N]
+    Ad = torch.from_numpy(Abuf).cuda()[1:].view(M, lda)[:, :K]
+    Bd = torch.from_numpy(Bbuf).cuda()[1:].view(K, ldb)[:, :N]
+    Cbuf = torch.full((M * ldc + 1,), float("nan"), device="cuda")
+    Cd = Cbuf[1:].view(M, ldc)[:, :N]
+    announce("parity padded/misaligned %s" % INAME[instance])
+    heal.heal_gemm_f32_instance(instance, Ad, Bd, out=Cd)
+    torch.cuda.synchronize()
+    _, S = orc.gemm3(A, B)
+    check_tolerance(Cd.cpu().numpy(), S, abs_product(A, B), "padded")
+    # the padding columns of C are untouched
+    assert torch.isnan(Cbuf[1:].view(M, ldc)[:, N:]).all()
+
+
+def test_k_zero_writes_zero_and_empty_is_noop():
+    announce("K=0 and empty products")
+    A = torch.empty((5, 0), device="cuda")
+    B = torch.empty((0, 7), device="cuda")
+    C = torch.full((5, 7), float("nan"), device="cuda")
+    heal.heal_gemm_f32(A, B, out=C)
+    torch.cuda.synchronize()
+    assert torch.equal(C, torch.zeros_like(C))
+    assert not torch.signbit(C).any()
+    A = torch.ones((0, 4), device="cuda")
+    B = torch.ones((4, 3), device="cuda")
+    C = heal.heal_gemm_f32(A, B)
+    assert C.shape == (0, 3)
+
+
+def test_nonfinite_inputs_match_oracle(orc):
+    """inf/NaN inputs give the oracle's inf/NaN pattern; finite outputs stay in tolerance."""
+    rng = np.random.default_rng(9)
+    A = rng.standard_normal((40, 70)).astype(np.float32)
+    B = rng.standard_normal((70, 50)).astype(np.float32)
+    A[3, 5] = np.inf
+    A[7, 9] = -np.inf
+    A[11, 0] = np.nan
+    B[20, 13] = np.inf
+    B[2, 2] = np.float32(3.4e38)      # finite, but rounds to +inf in bf16
+    Co, S = orc.gemm3(A, B)
+    fin = np.isfinite(Co)
+    absAB = abs_product(np.where(np.isfinite(A), A, 0), np.where(np.isfinite(B), B, 0))
+    for inst in INSTANCES:
+        announce("non-finite inputs %s" % INAME[inst])
+        C = gpu_gemm(A, B, inst)
+        assert np.array_equal(np.isnan(C), np.isnan(Co)), "NaN pattern differs"
+        assert np.array_equal(np.isinf(C), np.isinf(Co)), "inf pattern differs"
+        assert np.array_equal(C[np.isinf(Co)], Co[np.isinf(Co)]), "sign of inf differs"
+        err = np.abs(C[fin].astype(np.float64) - S[fin])
+        assert np.all(err <= 1e-5 * absAB[fin])
+
+
+# ---------------------------------------------------------------------------
+# the contract's workloads at full size (sampled rows against the oracle)
+# ---------------------------------------------------------------------------
+def _rows(M, n, seed):
+    rng = np.random.default_rng(seed)
+    r = {0, M - 1} | set(rng.choice(M, min(n, M), replace=False).tolist())
+    return np.array(sorted(r), dtype=np.int64)
+
+
+def test_config_square256_full(orc):
+    w = wl.WORKLOADS["square256"]
+    A, B = wl.make_inputs(w)
+    announce("config square256")
+    C = gpu_gemm(A, B)
+    _, S = orc.gemm3(A, B)
+    nw, ew = check_tolerance(C, S, abs_product(A, B), "square256")
+    print("square256 normwise %.3g elementwise %.3g" % (nw, ew))
+
+
+@pytest.mark.parametrize("name,nrows", [("decode", 16), ("prefill_up", 6), ("square8192", 4),
+                                        ("lm_head", 3)])
+def test_config_full_size_sampled(orc, name, nrows):
+    w = wl.WORKLOADS[name]
+    A, B = wl.make_inputs(w)
+    announce("config %s %dx%dx%d" % (name, w.M, w.N, w.K))
+    Ad, Bd = to_dev(A), to_dev(B)
+    C = heal.heal_gemm_f32(Ad, Bd)
+    torch.cuda.synchronize()
+    rows = _rows(w.M, nrows, w.seed)
+    Cr = C[torch.from_numpy(rows).cuda()].cpu().numpy()
+    del C, Ad, Bd
+    _, S = orc.gemm3(A, B, rows=rows)
+    nw, ew = check_tolerance(Cr, S, abs_product(A[rows], B), name)
+    print("%s rows %s normwise %.3g elementwise %.3g" % (name, rows.tolist(), nw, ew))
+
+
+def test_config_attention_sampled(orc):
+    w = wl.WORKLOADS["attn_scores"]
+    Q, Kh = wl.make_inputs(w)
+    announce("config attn_scores batched")
+    C = heal.heal_gemm_f32_strided_batched(to_dev(Q), to_dev(Kh), alpha=w.alpha, trans_b=True)
+    torch.cuda.synchronize()
+    alpha = float(np.float32(w.alpha))
+    for h in (0, 13, 31):
+        rows = _rows(w.M, 4, h)
+        Cr = C[h][torch.from_numpy(rows).cuda()].cpu().numpy()
+        B = np.ascontiguousarray(Kh[h].T)
+        _, S = orc.gemm3(Q[h], B, alpha=w.alpha, rows=rows)
+        check_tolerance(Cr, alpha * S, alpha * abs_product(Q[h][rows], B), "attn head %d" % h)
+
+
+# ---------------------------------------------------------------------------
+# bitwise invariants (GPU against itself)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["square8192", "decode", "attn_scores"])
+def test_bitwise_repro_10_runs(name):
+    w = wl.WORKLOADS[name]
+    A, B = wl.make_inputs(w)
+    Ad, Bd = to_dev(A), to_dev(B)
+    announce("bit-repro x10 %s" % name)
+    if name == "attn_scores":
+        run = lambda: heal.heal_gemm_f32_strided_batched(Ad, Bd, alpha=w.alpha, trans_b=True)
+    else:
+        run = lambda: heal.heal_gemm_f32(Ad, Bd)
+    ref = run()
+    # a concurrent product on another stream must not change the bits
+    side = torch.cuda.Stream()
+    for r in range(10):
+        if r % 2:
+            with torch.cuda.stream(side):
+                x = torch.randn(2048, 2048, device="cuda")
+                heal.heal_gemm_f32(x, x)
+        C = run()
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int32), ref.view(torch.int32)), "run %d differs" % r
+
+
+def test_batch_invariance_attention_all_m():
+    """Row i of C(Q[:M], K^T) is bitwise the same for every M = 1..2048 (head 0),
+    and for a ladder of M on the other heads."""
+    w = wl.WORKLOADS["attn_scores"]
+    Q, Kh = wl.make_inputs(w)
+    Qd, Kd = to_dev(Q), to_dev(Kh)
+    announce("batch invariance head 0, M=1..2048")
+    full = heal.heal_gemm_f32_strided_batched(Qd, Kd, alpha=w.alpha, trans_b=True)
+    fb = full.view(torch.int32)
+    for M in range(1, w.M + 1):
+        C = heal.heal_gemm_f32_strided_batched(Qd[0:1, :M], Kd[0:1], alpha=w.alpha, trans_b=True)
+        assert torch.equal(C.view(torch.int32)[0], fb[0, :M]), "head 0 differs at M=%d" % M
+    ladder = [1, 2, 3, 5, 8, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256, 257,
+              511, 512, 1023, 1024, 1025, 2047, 2048]
+    announce("batch invariance other heads, ladder of M")
+    for M in ladder:
+        C = heal.heal_gemm_f32_strided_batched(Qd[:, :M].contiguous(), Kd, alpha=w.alpha,
+                                               trans_b=True)
+        assert torch.equal(C.view(torch.int32), fb[:, :M]), "heads differ at M=%d" % M
+
+
+@pytest.mark.parametrize("shape", [(300, 257, 100), (64, 1000, 4096), (1000, 64, 513),
+                                   (16, 4096, 512)], ids=lambda s: "x".join(map(str, s)))
+def test_instances_bitwise_equal(shape):
+    M, N, K = shape
+    A = wl.random_matrix((M, K), seed=21)
+    B = wl.random_matrix((K, N), seed=22)
+    announce("instances bitwise %s" % (shape,))
+    outs = [gpu_gemm(A, B, inst) for inst in INSTANCES]
+    for inst, C in zip(INSTANCES[1:], outs[1:]):
+        assert np.array_equal(C.view(np.int32), outs[0].view(np.int32)), \
+            "%s differs from large" % INAME[inst]
+
+
+def test_entry_points_bitwise_equal():
+    M, N, K = 200, 300, 333
+    A = wl.random_matrix((M, K), seed=31)
+    B = wl.random_matrix((K, N), seed=32)
+    Ad, Bd = to_dev(A), to_dev(B)
+    announce("entry points bitwise")
+    C0 = heal.heal_gemm_f32(Ad, Bd)
+    C1 = heal.heal_gemm_f32_strided_batched(Ad[None], Bd[None], alpha=1.0, trans_b=False)[0]
+    C2 = heal.heal_gemm_f32_strided_batched(Ad[None], Bd.t().contiguous()[None], alpha=1.0,
+                                            trans_b=True)[0]
+    torch.cuda.synchronize()
+    assert torch.equal(C0.view(torch.int32), C1.view(torch.int32))
+    assert torch.equal(C0.view(torch.int32), C2.view(torch.int32))
+    # batch entries are independent products
+    A3 = torch.stack([Ad, Ad.flip(0)])
+    C3 = heal.heal_gemm_f32_strided_batched(A3, torch.stack([Bd, Bd]))
+    torch.cuda.synchronize()
+    assert torch.equal(C3[0].view(torch.int32), C0.view(torch.int32))
+    assert torch.equal(C3[1].view(torch.int32), C0.flip(0).view(torch.int32))
