@@ -7,7 +7,7 @@
  * products summed into an FP32 output) keeps a GEMM on 16-bit matrix units
  * while recovering the significand bits a single 16-bit cast would lose.
  * Here both FP32 operands are split into bfloat16 pairs
- *     hi = RNE_bf16(x),  lo = RNE_bf16(x - hi)      (lo = 0 if hi is not finite)
+ *     hi = RNE_bf16(x),  lo = RNE_bf16(x - hi)
  * and the product is
  *     C = hiA*hiB + hiA*loB + loA*hiB
  * accumulated in FP32 by bf16 MFMA instructions and written as FP32 (the
@@ -67,12 +67,15 @@ int heal_version(void);
  * paragraph: the FP32 input is decomposed into a 16-bit head and residual).
  *   x   : n FP32 values (device, read-only).
  *   hi  : n bf16 bit patterns, hi[i] = RNE_bf16(x[i]) (device, written).
- *   lo  : n bf16 bit patterns, lo[i] = RNE_bf16(x[i] - hi[i]), or +0 when
- *         hi[i] is infinite or NaN (device, written).
+ *   lo  : n bf16 bit patterns, lo[i] = RNE_bf16(x[i] - hi[i]) evaluated in
+ *         IEEE arithmetic (device, written).
  *   n   : number of elements, n >= 0 (n == 0 is a no-op).
  * The subtraction x - hi is exact, so |x - hi - lo| <= 2^-17 |x| for every
  * finite x that does not round to infinity.  hi and lo must not overlap x or
- * each other.  NaN inputs give a NaN hi (payload unspecified) and lo = +0.
+ * each other.  Non-finite inputs follow IEEE arithmetic: x = +/-inf gives
+ * hi = x and lo = NaN; a finite x that rounds to infinity gives lo = -/+inf;
+ * x = NaN gives NaN for both (payloads unspecified).  Any output of the GEMM
+ * that such an element reaches is therefore NaN.
  */
 heal_status_t heal_split_f32(const float *x, uint16_t *hi, uint16_t *lo, int64_t n,
                              hipStream_t stream);

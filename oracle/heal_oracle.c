@@ -21,9 +21,11 @@
  *     HEAL-Full: GEMM outputs are kept in FP32):  C = (float)(alpha * S).
  *
  * Readings where the paper is silent (each is listed in the design notes):
- *   - NaN input: hi is the canonical quiet NaN with the input's sign, lo = 0;
- *   - whenever hi is not finite (inf input, or a finite input that rounds to
- *     inf), lo = 0, so infinities and NaNs propagate as in an FP32 GEMM;
+ *   - the residual is evaluated exactly as defined, in IEEE arithmetic, for
+ *     every input: an infinite x gives hi = x and lo = RNE(inf - inf) = NaN,
+ *     a finite x that rounds to infinity gives lo = -/+inf, a NaN x gives NaN
+ *     for both; so every output such an input reaches is NaN;
+ *   - a NaN is rounded to the canonical quiet NaN with the NaN's sign;
  *   - no scaling of lo (bf16 has the FP32 exponent range, unlike the FP16
  *     variant of the paper, which scales its residual by 2^10).
  *
@@ -67,13 +69,9 @@ static void split_one(float x, uint16_t *hi, uint16_t *lo)
 {
     uint16_t h = oracle_bf16_rne(x);
     float hf = oracle_bf16_to_float(h);
-    uint16_t l = 0;
-    if (isfinite(hf)) {
-        float r = x - hf;          /* exact: |r| <= half an ulp of hi, on x's grid */
-        l = oracle_bf16_rne(r);
-    }
+    float r = x - hf;   /* exact for finite hi: |r| <= half a bf16 step of x, on x's grid */
     *hi = h;
-    *lo = l;
+    *lo = oracle_bf16_rne(r);
 }
 
 void oracle_split(const float *x, uint16_t *hi, uint16_t *lo, int64_t n)

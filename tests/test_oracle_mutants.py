@@ -26,8 +26,8 @@ MUTATIONS = [
     ("truncate_not_round", "if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u)))", "if (0)"),
     ("ties_away", "if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u)))", "if (dropped >= 0x8000u)"),
     ("ties_to_odd", "(dropped == 0x8000u && (kept & 1u))", "(dropped == 0x8000u && !(kept & 1u))"),
-    ("lo_not_zero_nonfinite", "if (isfinite(hf)) {", "if (1) {"),
-    ("lo_is_residual_truncated", "l = oracle_bf16_rne(r);", "l = (uint16_t)(bits_of(r) >> 16);"),
+    ("lo_zero_for_nonfinite_hi", "float r = x - hf;", "float r = isfinite(hf) ? x - hf : 0.0f;"),
+    ("lo_is_residual_truncated", "*lo = oracle_bf16_rne(r);", "*lo = (uint16_t)(bits_of(r) >> 16);"),
     ("nan_not_quiet", "return (uint16_t)(((u >> 16) & 0x8000u) | 0x7fc0u);", "return (uint16_t)(u >> 16);"),
     ("alpha_ignored", "c[j] = (float)((double)alpha * s[j]);", "c[j] = (float)s[j];"),
     ("alpha_after_round", "c[j] = (float)((double)alpha * s[j]);", "c[j] = alpha * (float)s[j];"),
