@@ -32,6 +32,17 @@ namespace {
 
 constexpr int kChunk = 32;  // K depth of one bf16 MFMA: the unit of the reduction order
 
+// Steady-state interleave: the split of the next stage starts after
+// SPLIT_AT/8 of the current stage's MFMA chunks, giving its global loads that
+// long to arrive.
+#ifndef HEAL_SCHED_SPLIT_AT
+#define HEAL_SCHED_SPLIT_AT 4
+#endif
+// Large instance: BM, BN, BK, WM, WN, threads
+#ifndef HEAL_LARGE_CFG
+#define HEAL_LARGE_CFG 256, 256, 32, 64, 128, 512
+#endif
+
 template <int BM, int BN, int BK, int WM, int WN, int NT>
 struct Tile {
     static_assert(BK % kChunk == 0, "stage depth must be whole MFMA chunks");
@@ -54,6 +65,18 @@ struct Tile {
     static constexpr int ITBT = (QBT + NT - 1) / NT;
     static constexpr int ITB = (BB + NT - 1) / NT;
 
+    static constexpr int LKQ = KQ == 8 ? 3 : KQ == 16 ? 4 : KQ == 32 ? 5 : -1;
+    static_assert(LKQ > 0, "stage depth must be 32, 64 or 128");
+    // LDS row of B column n.  With 64-byte rows the two halves of each
+    // 8-row group trade their odd/even rows when bit 2 of n is set, so the
+    // register-transposed B writes of one instruction (all lanes writing the
+    // same column offset nn) still land on both row parities, i.e. on all
+    // 32 banks.  A read pass covers whole 8-row groups, so reads are
+    // unaffected.
+    static __device__ __forceinline__ int brow(int n)
+    {
+        return ROWB == 64 ? n ^ ((n >> 2) & 1) : n;
+    }
     // byte offset of 4 consecutive k (k = 4*kq) of row `row` in a plane
     static __device__ __forceinline__ int quad_off(int row, int kq)
     {
@@ -99,18 +122,24 @@ gemm_bf16x3_kernel(GemmArgs p)
     // Work distribution of the loads (see the load lambdas below).
     constexpr int A_ROWS_PER_PASS = NT / T::KQ;          // A rows covered by one pass of NT threads
     constexpr int BT_ROWS_PER_PASS = NT / T::KQ;         // same for B stored N x K
-    constexpr int B_NQ = BN / 4;                         // 4-column groups per B row (B stored K x N)
-    constexpr int B_KQ_PER_PASS = NT / B_NQ;             // 4-row groups covered by one pass
-    static_assert(NT % T::KQ == 0 && NT % B_NQ == 0, "load distribution");
+    // B stored K x N: each thread loads a 4 (k) x 4 (n) block, which it
+    // transposes in registers.  Lane bits 1..LKQ pick the k-quad, lane bit 0
+    // and the remaining lane and wave bits the 4-column group, so that one
+    // write instruction's 16-lane passes cover all 16 eight-byte bank slots
+    // and one load instruction reads whole 128-byte row segments.
+    constexpr int B_NQ_PER_PASS = NT / T::KQ;            // 4-column groups per pass
+    static_assert(NT % T::KQ == 0 && T::KQ <= 32, "load distribution");
     static_assert((A_ROWS_PER_PASS / T::RPW) % (T::SWM + 1) == 0 || T::ITA == 1,
                   "swizzle must repeat across A passes");
     static_assert((BT_ROWS_PER_PASS / T::RPW) % (T::SWM + 1) == 0 || T::ITBT == 1,
                   "swizzle must repeat across B passes");
-    static_assert(T::ITB == 1 || ((B_KQ_PER_PASS / 2) % (T::SWM + 1)) == 0,
-                  "swizzle must repeat across B passes");
     static_assert((16 / T::RPW) % (T::SWM + 1) == 0, "swizzle must repeat every 16 rows");
 
-    __shared__ __attribute__((aligned(16))) char smem[2 * T::STAGE];
+    // Two LDS stage buffers as distinct objects, so the compiler can tell the
+    // split's writes into one from the fragment reads of the other and
+    // interleave them.
+    __shared__ __attribute__((aligned(16))) char smem0[T::STAGE];
+    __shared__ __attribute__((aligned(16))) char smem1[T::STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -139,7 +168,12 @@ gemm_bf16x3_kernel(GemmArgs p)
 
     const int64_t M = p.M, N = p.N, K = p.K;
     const int64_t nk = (K + BK - 1) / BK;
-    const bool interior = VEC && m0 + BM <= M && n0 + BN <= N;
+    // interior: whole tile in range, 16-byte aligned rows, and every byte
+    // offset of a tile (A, B stored N x K) or of a stage (B stored K x N)
+    // below 2^31, so the fast path can use buffer loads with 32-bit offsets.
+    const bool interior = VEC && m0 + BM <= M && n0 + BN <= N &&
+                          (int64_t)BM * p.lda * 4 < 0x7fffffffLL &&
+                          (int64_t)(TRANS_B ? BN : BK) * p.ldb * 4 < 0x7fffffffLL;
 
     const int wm = wave % T::WAVES_M;
     const int wn = wave / T::WAVES_M;
@@ -150,8 +184,9 @@ gemm_bf16x3_kernel(GemmArgs p)
     // per-thread load coordinates (fixed for the whole tile)
     const int a_row = tid / T::KQ;                 // + pass * A_ROWS_PER_PASS
     const int a_kq = tid % T::KQ;
-    const int b_nq = tid % B_NQ;                   // B stored K x N
-    const int b_kq = tid / B_NQ;                   // + pass * B_KQ_PER_PASS
+    const int b_kq = (lane >> 1) & (T::KQ - 1);   // B stored K x N
+    const int b_nq = (lane & 1) | ((lane >> (1 + T::LKQ)) << 1) | (wave << (6 - T::LKQ));
+                                                   // + pass * B_NQ_PER_PASS
     const int a_st = T::quad_off(a_row, a_kq);     // LDS store offsets
     const int bt_st = a_st;                        // B stored N x K uses the A pattern
 
@@ -172,27 +207,39 @@ gemm_bf16x3_kernel(GemmArgs p)
         f32x4 ra[T::ITA];
         f32x4 rb[TRANS_B ? T::ITBT : T::ITB][TRANS_B ? 1 : 4];
 
-        // Full stage of an interior tile: unconditional 16-byte loads.
+        // Full stage of an interior tile: buffer loads, one 32-bit VGPR offset
+        // per operand and thread; stage and pass offsets are scalar.
+        constexpr int kRsrcFlags = 0x00020000;   // raw buffer, 32-bit data format
+        const __amdgpu_buffer_rsrc_t rsrc_a = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(A + m0 * p.lda), (short)0, 0x7fffffff, kRsrcFlags);
+        const int voff_a = (a_row * (int)p.lda + 4 * a_kq) * 4;
+        const int voff_b = TRANS_B ? (a_row * (int)p.ldb + 4 * a_kq) * 4
+                                   : (4 * b_kq * (int)p.ldb + 4 * b_nq) * 4;
         auto load_stage_fast = [&](int64_t k0) {
 #pragma unroll
             for (int it = 0; it < T::ITA; ++it)
                 if (T::QA % NT == 0 || it * NT + tid < T::QA)
-                    ra[it] = *reinterpret_cast<const f32x4 *>(
-                        pa + (int64_t)(it * A_ROWS_PER_PASS) * p.lda + k0);
+                    ra[it] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                        rsrc_a, voff_a, (int)(k0 * 4) + it * A_ROWS_PER_PASS * (int)p.lda * 4, 0));
             if (TRANS_B) {
+                const __amdgpu_buffer_rsrc_t rsrc_b = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<float *>(B + n0 * p.ldb), (short)0, 0x7fffffff, kRsrcFlags);
 #pragma unroll
                 for (int it = 0; it < T::ITBT; ++it)
                     if (T::QBT % NT == 0 || it * NT + tid < T::QBT)
-                        rb[it][0] = *reinterpret_cast<const f32x4 *>(
-                            pb + (int64_t)(it * BT_ROWS_PER_PASS) * p.ldb + k0);
+                        rb[it][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                            rsrc_b, voff_b,
+                            (int)(k0 * 4) + it * BT_ROWS_PER_PASS * (int)p.ldb * 4, 0));
             } else {
+                const __amdgpu_buffer_rsrc_t rsrc_b = __builtin_amdgcn_make_buffer_rsrc(
+                    const_cast<float *>(B + k0 * p.ldb + n0), (short)0, 0x7fffffff, kRsrcFlags);
 #pragma unroll
                 for (int it = 0; it < T::ITB; ++it)
-                    if (T::BB % NT == 0 || it * NT + tid < T::BB)
+                    if ((BN / 4) % B_NQ_PER_PASS == 0 || b_nq + it * B_NQ_PER_PASS < BN / 4)
 #pragma unroll
                         for (int kk = 0; kk < 4; ++kk)
-                            rb[it][kk] = *reinterpret_cast<const f32x4 *>(
-                                pb + (k0 + 4 * it * B_KQ_PER_PASS + kk) * p.ldb);
+                            rb[it][kk] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                rsrc_b, voff_b, kk * (int)p.ldb * 4 + it * B_NQ_PER_PASS * 16, 0));
             }
         };
 
@@ -216,72 +263,117 @@ gemm_bf16x3_kernel(GemmArgs p)
             } else {
 #pragma unroll
                 for (int it = 0; it < T::ITB; ++it)
-                    if (T::BB % NT == 0 || it * NT + tid < T::BB)
+                    if ((BN / 4) % B_NQ_PER_PASS == 0 || b_nq + it * B_NQ_PER_PASS < BN / 4)
 #pragma unroll
                         for (int kk = 0; kk < 4; ++kk) {
-                            const int64_t kr = k0 + 4 * (it * B_KQ_PER_PASS + b_kq) + kk;
+                            const int64_t kr = k0 + 4 * b_kq + kk;
                             rb[it][kk] = load_quad_checked<VEC>(
-                                pb + (k0 + 4 * it * B_KQ_PER_PASS + kk) * p.ldb, kr < K,
-                                n0 + 4 * b_nq, N);
+                                pb + (k0 + kk) * p.ldb + 4 * it * B_NQ_PER_PASS, kr < K,
+                                n0 + 4 * (b_nq + it * B_NQ_PER_PASS), N);
                         }
             }
         };
 
-        auto store_stage = [&](int buf) {
-            char *s = smem + buf * T::STAGE;
+        // Split units: one 4-element quad (two split2 calls, two 8-byte LDS
+        // writes per plane pair) of this thread's staged data.
+        constexpr int NU = T::ITA + (TRANS_B ? T::ITBT : 4 * T::ITB);
+        auto store_unit = [&](char *s, const int u) {
             char *a_hi = s, *a_lo = s + T::A_PLANE;
             char *b_hi = s + 2 * T::A_PLANE, *b_lo = b_hi + T::B_PLANE;
-#pragma unroll
-            for (int it = 0; it < T::ITA; ++it) {
+            uint32_t h0, l0, h1, l1;
+            if (u < T::ITA) {
+                const int it = u;
                 if (T::QA % NT == 0 || it * NT + tid < T::QA) {
-                    uint32_t h0, l0, h1, l1;
                     split2(ra[it].x, ra[it].y, h0, l0);
                     split2(ra[it].z, ra[it].w, h1, l1);
                     const int off = a_st + it * A_ROWS_PER_PASS * T::ROWB;
                     store_pair(a_hi, off, h0, h1);
                     store_pair(a_lo, off, l0, l1);
                 }
-            }
-            if (TRANS_B) {
-#pragma unroll
-                for (int it = 0; it < T::ITBT; ++it) {
-                    if (T::QBT % NT == 0 || it * NT + tid < T::QBT) {
-                        uint32_t h0, l0, h1, l1;
-                        split2(rb[it][0].x, rb[it][0].y, h0, l0);
-                        split2(rb[it][0].z, rb[it][0].w, h1, l1);
-                        const int off = bt_st + it * BT_ROWS_PER_PASS * T::ROWB;
-                        store_pair(b_hi, off, h0, h1);
-                        store_pair(b_lo, off, l0, l1);
-                    }
+            } else if (TRANS_B) {
+                const int it = u - T::ITA;
+                if (T::QBT % NT == 0 || it * NT + tid < T::QBT) {
+                    split2(rb[it][0].x, rb[it][0].y, h0, l0);
+                    split2(rb[it][0].z, rb[it][0].w, h1, l1);
+                    const int off = bt_st + it * BT_ROWS_PER_PASS * T::ROWB;
+                    store_pair(b_hi, off, h0, h1);
+                    store_pair(b_lo, off, l0, l1);
                 }
             } else {
-#pragma unroll
-                for (int it = 0; it < T::ITB; ++it) {
-                    if (T::BB % NT == 0 || it * NT + tid < T::BB) {
-                        // register transpose: column nn of the 4x4 block is 4 consecutive k
-#pragma unroll
-                        for (int nn = 0; nn < 4; ++nn) {
-                            uint32_t h0, l0, h1, l1;
-                            split2(rb[it][0][nn], rb[it][1][nn], h0, l0);
-                            split2(rb[it][2][nn], rb[it][3][nn], h1, l1);
-                            const int off = T::quad_off(4 * b_nq + nn, b_kq + it * B_KQ_PER_PASS);
-                            store_pair(b_hi, off, h0, h1);
-                            store_pair(b_lo, off, l0, l1);
-                        }
-                    }
+                // register transpose: column nn of the 4x4 block is 4 consecutive k
+                const int it = (u - T::ITA) / 4, nn = (u - T::ITA) % 4;
+                if ((BN / 4) % B_NQ_PER_PASS == 0 || b_nq + it * B_NQ_PER_PASS < BN / 4) {
+                    split2(rb[it][0][nn], rb[it][1][nn], h0, l0);
+                    split2(rb[it][2][nn], rb[it][3][nn], h1, l1);
+                    const int off = T::quad_off(T::brow(4 * (b_nq + it * B_NQ_PER_PASS) + nn), b_kq);
+                    store_pair(b_hi, off, h0, h1);
+                    store_pair(b_lo, off, l0, l1);
                 }
             }
         };
 
-        auto compute_stage = [&](int buf) {
-            const char *s = smem + buf * T::STAGE;
+        auto store_stage = [&](char *s) {
+#pragma unroll
+            for (int u = 0; u < NU; ++u) store_unit(s, u);
+        };
+
+        // One steady-state stage of an interior tile, software-interleaved:
+        // the stage's MFMAs are cut into chunks (one 16-column block of B and
+        // one 32-deep k step each), and the split of the next stage's data is
+        // spread over the later chunks, so that VALU work issues while the
+        // matrix cores run.  Scheduling barriers keep the chunks apart.
+        auto stage_fast = [&](const char *cur, char *nxt, int64_t k_next) {
+            load_stage_fast(k_next);
+            const char *a_hi = cur, *a_lo = cur + T::A_PLANE;
+            const char *b_hi = cur + 2 * T::A_PLANE, *b_lo = b_hi + T::B_PLANE;
+            constexpr int NJ = WN / 16, KS = BK / kChunk, NC = NJ * KS;
+            constexpr int C0s = NC * HEAL_SCHED_SPLIT_AT / 8;
+            constexpr int C0 = C0s < NC ? C0s : NC - 1;  // first chunk that splits
+            bf16x8 ah[WM / 16], al[WM / 16], bh[2], bl[2];
+            auto read_b = [&](int c, int slot) {
+                const int off = T::chunk_off(TRANS_B ? wn * WN + fr : T::brow(wn * WN + fr),
+                                             (c / NJ) * 4 + fg) + (c % NJ) * 16 * T::ROWB;
+                bh[slot] = *reinterpret_cast<const bf16x8 *>(b_hi + off);
+                bl[slot] = *reinterpret_cast<const bf16x8 *>(b_lo + off);
+            };
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                const int ks = c / NJ, j = c % NJ;
+                if (j == 0) {
+                    const int a_off = T::chunk_off(wm * WM + fr, ks * 4 + fg);
+#pragma unroll
+                    for (int i = 0; i < WM / 16; ++i) {
+                        ah[i] = *reinterpret_cast<const bf16x8 *>(a_hi + a_off + i * 16 * T::ROWB);
+                        al[i] = *reinterpret_cast<const bf16x8 *>(a_lo + a_off + i * 16 * T::ROWB);
+                    }
+                }
+                if (c == 0) read_b(0, 0);
+                if (c + 1 < NC) read_b(c + 1, (c + 1) & 1);
+                const int sl = c & 1;
+#pragma unroll
+                for (int i = 0; i < WM / 16; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[sl], ah[i], acc[j][i], 0, 0, 0);
+#pragma unroll
+                for (int i = 0; i < WM / 16; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl[sl], ah[i], acc[j][i], 0, 0, 0);
+#pragma unroll
+                for (int i = 0; i < WM / 16; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[sl], al[i], acc[j][i], 0, 0, 0);
+#pragma unroll
+                for (int u = 0; u < NU; ++u)
+                    if (C0 + (u * (NC - C0)) / NU == c) store_unit(nxt, u);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+
+        auto compute_stage = [&](const char *s) {
             const char *a_hi = s, *a_lo = s + T::A_PLANE;
             const char *b_hi = s + 2 * T::A_PLANE, *b_lo = b_hi + T::B_PLANE;
 #pragma unroll
             for (int ks = 0; ks < BK / kChunk; ++ks) {
                 const int c = ks * 4 + fg;
                 const int a_off = T::chunk_off(wm * WM + fr, c);
-                const int b_off = T::chunk_off(wn * WN + fr, c);
+                const int b_off = T::chunk_off(TRANS_B ? wn * WN + fr : T::brow(wn * WN + fr), c);
                 bf16x8 ah[WM / 16], al[WM / 16];
 #pragma unroll
                 for (int i = 0; i < WM / 16; ++i) {
@@ -312,24 +404,37 @@ gemm_bf16x3_kernel(GemmArgs p)
         if (nk > 0) {
             if (VEC && interior && BK <= K) load_stage_fast(0);
             else load_stage_checked(0);
-            store_stage(0);
+            store_stage(smem0);
             __syncthreads();
         }
         if (VEC && interior) {
+            // two stages per trip so that each buffer is a compile-time choice
             const int64_t nk_full = K / BK;  // stages without a K tail
-            for (; kt + 1 < nk_full; ++kt) {
-                const int buf = (int)(kt & 1);
-                load_stage_fast((kt + 1) * BK);
-                if (computes) compute_stage(buf);
-                store_stage(buf ^ 1);
+            for (; kt + 2 < nk_full; kt += 2) {
+                if (T::CWAVES * 64 == NT) {
+                    stage_fast(smem0, smem1, (kt + 1) * BK);
+                } else {
+                    load_stage_fast((kt + 1) * BK);
+                    if (computes) compute_stage(smem0);
+                    store_stage(smem1);
+                }
+                __syncthreads();
+                if (T::CWAVES * 64 == NT) {
+                    stage_fast(smem1, smem0, (kt + 2) * BK);
+                } else {
+                    load_stage_fast((kt + 2) * BK);
+                    if (computes) compute_stage(smem1);
+                    store_stage(smem0);
+                }
                 __syncthreads();
             }
         }
         for (; kt < nk; ++kt) {
-            const int buf = (int)(kt & 1);
+            char *cur = (kt & 1) ? smem1 : smem0;
+            char *nxt = (kt & 1) ? smem0 : smem1;
             if (kt + 1 < nk) load_stage_checked((kt + 1) * BK);
-            if (computes) compute_stage(buf);
-            if (kt + 1 < nk) store_stage(buf ^ 1);
+            if (computes) compute_stage(cur);
+            if (kt + 1 < nk) store_stage(nxt);
             __syncthreads();
         }
 
@@ -397,7 +502,7 @@ hipError_t launch_gemm(int instance, const GemmArgs &a, bool trans_b, bool use_a
 {
     switch (instance) {
     case HEAL_INSTANCE_LARGE:
-        return launch_tile<256, 256, 32, 64, 128, 512>(a, trans_b, use_alpha, stream);
+        return launch_tile<HEAL_LARGE_CFG>(a, trans_b, use_alpha, stream);
     case HEAL_INSTANCE_MEDIUM:
         return launch_tile<128, 128, 32, 64, 64, 256>(a, trans_b, use_alpha, stream);
     case HEAL_INSTANCE_SKINNY:
