@@ -1,19 +1,34 @@
 """Benchmark of the bf16x3 compensated GEMM (heal_gemm_f32) on one MI355X.
 
-One step = one compensated product over the whole workload, inputs resident in
-HBM.  Default workload: M = N = K = 8192, A and B ~ N(0, 1) FP32.
+One step = one compensated product over the whole workload (every step of the
+method: split, three bf16 products, FP32 accumulation and output, all inside
+one kernel launch), inputs resident in HBM when the timed region starts.
+Default workload: M = N = K = 8192, A and B ~ N(0, 1) FP32, the square case the
+throughput target is quoted on.  Other workloads (--workload) are the
+LLM-layer shapes of the parity tests.
+
 Prints ONE JSON line:
-  value        FP32-equivalent TFLOP/s, 2*M*N*K per step / time
-  roofline     the GEMM kernel against the bf16 dense MFMA peak: it executes
-               6*M*N*K bf16 flops per launch (three products), so
-               frac = (6MNK / t) / peak = (2MNK / t) / (peak / 3)
-  cpu_baseline the CPU oracle on a bounded row sample of the same product
-  comparison   MI355X native FP32 GEMM (torch.matmul, no TF32) on the same inputs
+  value        FP32-equivalent TFLOP/s, 2*M*N*K*batch per step / time per step
+  roofline     the GEMM kernel (the only kernel of a step) against its bound:
+                 mfma: 6*M*N*K bf16 flops per launch (three products) over the
+                       bf16 dense MFMA peak, so frac = value / (peak / 3);
+                 hbm:  FP32 A, B read once and C written once per launch over
+                       the 8 TB/s HBM peak;
+               the launch duration is the mean over the timed launches, taken
+               with HIP events on the stream the kernel runs on.  traffic is
+               the HBM bytes per launch measured by FETCH_SIZE / WRITE_SIZE
+               counters (scaled by a plain copy of known size), taken from
+               profiles/traffic.json only while the kernel sources are the
+               ones it was measured on, else null.
+  cpu_baseline the CPU oracle timed on a bounded row sample of the same product
+  comparison   MI355X native FP32 GEMM (torch.matmul, TF32 off) on the same inputs
   bit_repro    every timed step's output bitwise equal to the first
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
 """
 import argparse
+import hashlib
 import json
+import math
 import os
 import sys
 import time
@@ -25,6 +40,8 @@ sys.path.insert(0, ROOT)
 
 BF16_DENSE_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 bf16 flop/clk/CU (MI355X, dense)
 HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCES = ["heal_gemm.hip", "heal_device.h", "heal_internal.h"]
 
 
 def parse():
@@ -36,17 +53,37 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU oracle sample")
-    ap.add_argument("--traffic", default=None,
-                    help="JSON file with measured HBM bytes per launch for this workload")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed region, copy a 1 GiB buffer 3 times (a plain copy "
+                         "kernel of known size, for scaling HBM byte counters)")
     return ap.parse_args()
 
 
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_21023_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch from counters, if measured on the current kernel sources."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        t = json.load(f)
+    e = t.get("workloads", {}).get(workload)
+    if not e or t.get("kernel_source_sha") != kernel_source_hash():
+        return None
+    return e["fetch_kib"] * 1024.0 * t["read_factor"] + e["write_kib"] * 1024.0 * t["write_factor"]
+
+
 def cpu_baseline(w, A, B, target_s):
-    """Time the CPU oracle on the first R rows of the product, R sized to ~target_s."""
+    """Time the CPU oracle on the first R rows of the product, R grown to ~target_s."""
     from oracle import oracle
     orc = oracle.default()
     rows = 1
-    t = 0.0
     while True:
         t0 = time.perf_counter()
         orc.gemm3(A[:rows], B)
@@ -55,18 +92,19 @@ def cpu_baseline(w, A, B, target_s):
             break
         grow = max(2, int(target_s / max(t, 1e-3)))
         rows = min(A.shape[0], rows * grow)
-    flops = 2.0 * rows * w.N * w.K * w.batch
-    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": orc.num_threads(),
+    flops = 2.0 * rows * B.shape[1] * B.shape[0]
+    return {"value": round(flops / t / 1e12, 5), "unit": "TFLOP/s", "cores": orc.num_threads(),
             "kind": "oracle", "seconds": round(t, 3),
-            "sample": "first %d of %d rows of the %s product (%dx%dx%d), FP64 accumulation, "
-                      "B split included" % (rows, w.M, w.name, rows, w.N, w.K)}
+            "sample": "first %d of %d rows of one %s product (%dx%dx%d of the %d-entry batch), "
+                      "split of B included, FP64 accumulation" % (
+                          rows, A.shape[0], w.name, rows, B.shape[1], B.shape[0], w.batch)}
 
 
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: the compensated GEMM is a single-GPU kernel "
-              "and this build has no multi-GPU path (--gpus %d requested)" % args.gpus,
+        print("bench.py runs on exactly one GPU: the compensated GEMM is measured on one "
+              "GPU's share and there is no multi-GPU path (--gpus %d requested)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
 
@@ -78,36 +116,43 @@ def main():
     A, B = wl.make_inputs(w)
     torch.cuda.init()
     dev = torch.device("cuda:0")
-    Ad = torch.from_numpy(A).to(dev)
-    Bd = torch.from_numpy(B).to(dev)
     batched = w.trans_b or w.batch > 1
-    if batched:
-        Cd = torch.empty((w.batch, w.M, w.N), dtype=torch.float32, device=dev)
-        run = lambda out: heal.heal_gemm_f32_strided_batched(Ad, Bd, alpha=w.alpha,
-                                                             trans_b=w.trans_b, out=out)
-    else:
-        Cd = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
-        run = lambda out: heal.heal_gemm_f32(Ad, Bd, out=out)
-    first = torch.empty_like(Cd)
+    # Rotate through copies of the operands so that HBM-bound shapes are not
+    # served from the 256 MB Infinity Cache: at least 1 GiB of inputs in turn.
+    n_rot = int(min(16, max(1, math.ceil(float(1 << 30) / w.algorithmic_bytes))))
+    sets = []
+    for _ in range(n_rot):
+        Ad = torch.from_numpy(A).to(dev)
+        Bd = torch.from_numpy(B).to(dev)
+        shape = (w.batch, w.M, w.N) if batched else (w.M, w.N)
+        sets.append((Ad, Bd, torch.empty(shape, dtype=torch.float32, device=dev)))
 
-    for _ in range(args.warmup):
-        run(Cd)
-    run(first)
+    def run(i):
+        Ad, Bd, Cd = sets[i % n_rot]
+        if batched:
+            heal.heal_gemm_f32_strided_batched(Ad, Bd, alpha=w.alpha, trans_b=w.trans_b, out=Cd)
+        else:
+            heal.heal_gemm_f32(Ad, Bd, out=Cd)
+
+    for i in range(args.warmup):
+        run(i)
+    run(0)
     torch.cuda.synchronize()
+    first = sets[0][2].clone()
 
     stream = torch.cuda.current_stream()
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    identical = True
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         starts[i].record(stream)
-        run(Cd)
+        run(i)
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    identical = bool(torch.equal(Cd.view(torch.int32), first.view(torch.int32)))
+    identical = all(bool(torch.equal(s[2].view(torch.int32), first.view(torch.int32)))
+                    for s in sets[:min(n_rot, args.steps)])
     launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     total_ms = starts[0].elapsed_time(ends[-1])
     ms_per_step = total_ms / args.steps
@@ -116,21 +161,29 @@ def main():
     flops = w.flops
     value = flops / (ms_per_step * 1e-3) / 1e12
     mfma_flops = 3.0 * flops
-    achieved = mfma_flops / (avg_launch_ms * 1e-3) / 1e12
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            traffic = json.load(f).get(w.name)
-    roofline = {"bound": "mfma", "achieved": round(achieved, 2),
-                "peak": BF16_DENSE_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / BF16_DENSE_PEAK_TFLOPS, 4), "traffic": traffic,
-                "kernel": "gemm_bf16x3_kernel (large instance)",
-                "per_launch": "6*M*N*K bf16 MFMA flops = %.4g" % mfma_flops}
+    t_mfma = mfma_flops / (BF16_DENSE_PEAK_TFLOPS * 1e12)
+    t_hbm = w.algorithmic_bytes / (HBM_PEAK_GBS * 1e9)
+    traffic = measured_traffic(w.name)
+    if t_mfma >= t_hbm:
+        achieved = mfma_flops / (avg_launch_ms * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 2),
+                    "peak": BF16_DENSE_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / BF16_DENSE_PEAK_TFLOPS, 4)}
+        per_launch = "6*M*N*K*batch bf16 MFMA flops = %.4g" % mfma_flops
+    else:
+        achieved = w.algorithmic_bytes / (avg_launch_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+        per_launch = "4*(M*K + K*N + M*N)*batch bytes = %.4g" % w.algorithmic_bytes
+    roofline.update({"traffic": None if traffic is None else round(traffic),
+                     "kernel": "gemm_bf16x3_kernel, instance %d" % heal.select_instance(w.M, w.N),
+                     "per_launch": per_launch, "avg_launch_us": round(avg_launch_ms * 1e3, 2)})
 
     # MI355X native FP32 GEMM on the same inputs, TF32 off
     torch.backends.cuda.matmul.allow_tf32 = False
     torch.set_float32_matmul_precision("highest")
-    mm = (lambda: torch.matmul(Ad, Bd.transpose(-1, -2))) if batched else (lambda: Ad @ Bd)
+    Ad, Bd, _ = sets[0]
+    mm = (lambda: torch.matmul(Ad, Bd.transpose(-1, -2))) if w.trans_b else (lambda: Ad @ Bd)
     for _ in range(3):
         mm()
     torch.cuda.synchronize()
@@ -148,9 +201,8 @@ def main():
     cpu = None
     if not args.no_cpu:
         Ah = A[0] if batched else A
-        Bh = np.ascontiguousarray(B[0].T) if batched else B
-        wc = wl.Workload(w.name, w.M, w.N, w.K, w.seed)
-        cpu = cpu_baseline(wc, Ah, Bh, args.cpu_seconds)
+        Bh = np.ascontiguousarray(B[0].T) if w.trans_b else (B[0] if batched else B)
+        cpu = cpu_baseline(w, Ah, Bh, args.cpu_seconds)
 
     line = {
         "metric": "FP32-equiv TFLOP/s of compensated GEMM; % of bf16 MFMA peak/3; bit-repro",
@@ -167,15 +219,24 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "batch": w.batch,
                    "trans_b": w.trans_b, "alpha": w.alpha, "seed": w.seed,
-                   "inputs": w.note},
+                   "inputs": w.note, "operand_copies_rotated": n_rot},
         "pct_of_bf16_peak_div3": round(100.0 * value / (BF16_DENSE_PEAK_TFLOPS / 3), 2),
-        "bit_repro": {"runs": args.steps + 1, "identical": identical},
+        "hbm_gbs": round(w.algorithmic_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "bit_repro": {"runs": args.steps + args.warmup + 1, "identical": identical},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "comparison": comparison,
         "wall_s": round(wall, 3),
     }
     print(json.dumps(line))
+    sys.stdout.flush()
+
+    if args.copy_calibration:
+        src = torch.ones(256 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

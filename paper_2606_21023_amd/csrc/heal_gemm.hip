@@ -38,6 +38,10 @@ constexpr int kChunk = 32;  // K depth of one bf16 MFMA: the unit of the reducti
 #ifndef HEAL_SCHED_SPLIT_AT
 #define HEAL_SCHED_SPLIT_AT 4
 #endif
+// Tile rows per rasterisation group (L2 reuse of B panels across an XCD).
+#ifndef HEAL_GROUP_M
+#define HEAL_GROUP_M 8
+#endif
 // Large instance: BM, BN, BK, WM, WN, threads
 #ifndef HEAL_LARGE_CFG
 #define HEAL_LARGE_CFG 256, 256, 32, 64, 128, 512
@@ -158,7 +162,7 @@ gemm_bf16x3_kernel(GemmArgs p)
         const int64_t x = bid & 7, i = bid >> 3, q = nb >> 3, r = nb & 7;
         bid = x * q + (x < r ? x : r) + i;
     }
-    constexpr int GM = 8;
+    constexpr int GM = HEAL_GROUP_M;
     const int64_t group = bid / (GM * tiles_n);
     const int64_t first_m = group * GM;
     const int64_t gm = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
