@@ -41,7 +41,11 @@ sys.path.insert(0, ROOT)
 BF16_DENSE_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 bf16 flop/clk/CU (MI355X, dense)
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = ["heal_gemm.hip", "heal_device.h", "heal_internal.h"]
+KERNEL_SOURCES = ["heal_gemm.hip", "heal_gemm_large.hip", "heal_device.h", "heal_internal.h"]
+# the kernel each instance of heal_gemm_f32 launches (16-byte aligned operands)
+KERNEL_NAMES = {1: "gemm_large_kernel (256x256 tiles, 4 waves)",
+                2: "gemm_bf16x3_kernel<128,128,32,64,64,256> (medium)",
+                3: "gemm_bf16x3_kernel (skinny, M <= 64)"}
 
 
 def parse():
@@ -176,7 +180,7 @@ def main():
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
         per_launch = "4*(M*K + K*N + M*N)*batch bytes = %.4g" % w.algorithmic_bytes
     roofline.update({"traffic": None if traffic is None else round(traffic),
-                     "kernel": "gemm_bf16x3_kernel, instance %d" % heal.select_instance(w.M, w.N),
+                     "kernel": KERNEL_NAMES.get(heal.select_instance(w.M, w.N), "?"),
                      "per_launch": per_launch, "avg_launch_us": round(avg_launch_ms * 1e3, 2)})
 
     # MI355X native FP32 GEMM on the same inputs, TF32 off

@@ -4,6 +4,13 @@
 #include <stdint.h>
 #include <hip/hip_runtime.h>
 
+// Tile rows per rasterisation group of the tiled GEMM kernels: consecutive
+// workgroups of one XCD walk GM tile rows before moving to the next tile
+// column, so that they share A and B panels in that XCD's L2.
+#ifndef HEAL_GROUP_M
+#define HEAL_GROUP_M 8
+#endif
+
 namespace heal {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));

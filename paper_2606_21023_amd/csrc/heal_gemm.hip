@@ -38,10 +38,6 @@ constexpr int kChunk = 32;  // K depth of one bf16 MFMA: the unit of the reducti
 #ifndef HEAL_SCHED_SPLIT_AT
 #define HEAL_SCHED_SPLIT_AT 4
 #endif
-// Tile rows per rasterisation group (L2 reuse of B panels across an XCD).
-#ifndef HEAL_GROUP_M
-#define HEAL_GROUP_M 8
-#endif
 // Large instance: BM, BN, BK, WM, WN, threads
 #ifndef HEAL_LARGE_CFG
 #define HEAL_LARGE_CFG 256, 256, 32, 64, 128, 512
@@ -506,6 +502,7 @@ hipError_t launch_gemm(int instance, const GemmArgs &a, bool trans_b, bool use_a
 {
     switch (instance) {
     case HEAL_INSTANCE_LARGE:
+        if (large_kernel_applies(a, trans_b)) return launch_gemm_large(a, trans_b, use_alpha, stream);
         return launch_tile<HEAL_LARGE_CFG>(a, trans_b, use_alpha, stream);
     case HEAL_INSTANCE_MEDIUM:
         return launch_tile<128, 128, 32, 64, 64, 256>(a, trans_b, use_alpha, stream);

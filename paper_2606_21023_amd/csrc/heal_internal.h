@@ -27,6 +27,12 @@ struct GemmArgs {
 hipError_t launch_gemm(int instance, const GemmArgs &args, bool trans_b, bool use_alpha,
                        hipStream_t stream);
 
+// The dedicated large-tile kernel (heal_gemm_large.hip): 256 x 256 tiles,
+// 16-byte operand rows.  large_kernel_applies tells whether it can run a call.
+bool large_kernel_applies(const GemmArgs &args, bool trans_b);
+hipError_t launch_gemm_large(const GemmArgs &args, bool trans_b, bool use_alpha,
+                             hipStream_t stream);
+
 hipError_t launch_split(const float *x, uint16_t *hi, uint16_t *lo, int64_t n, hipStream_t stream);
 
 }  // namespace heal
