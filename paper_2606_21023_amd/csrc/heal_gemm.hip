@@ -39,6 +39,18 @@ constexpr int kChunk = 32;  // K depth of one bf16 MFMA: the unit of the reducti
 #define HEAL_SCHED_SPLIT_AT 4
 #endif
 // Large instance: BM, BN, BK, WM, WN, threads
+#ifndef HEAL_MEDIUM_CFG
+#define HEAL_MEDIUM_CFG 128, 128, 32, 64, 64, 256
+#endif
+#ifndef HEAL_SKINNY16_CFG
+#define HEAL_SKINNY16_CFG 16, 64, 64, 16, 16, 256
+#endif
+#ifndef HEAL_SKINNY32_CFG
+#define HEAL_SKINNY32_CFG 32, 64, 64, 32, 16, 256
+#endif
+#ifndef HEAL_SKINNY64_CFG
+#define HEAL_SKINNY64_CFG 64, 64, 64, 64, 16, 256
+#endif
 #ifndef HEAL_LARGE_CFG
 #define HEAL_LARGE_CFG 256, 256, 32, 64, 128, 512
 #endif
@@ -505,11 +517,12 @@ hipError_t launch_gemm(int instance, const GemmArgs &a, bool trans_b, bool use_a
         if (large_kernel_applies(a, trans_b)) return launch_gemm_large(a, trans_b, use_alpha, stream);
         return launch_tile<HEAL_LARGE_CFG>(a, trans_b, use_alpha, stream);
     case HEAL_INSTANCE_MEDIUM:
-        return launch_tile<128, 128, 32, 64, 64, 256>(a, trans_b, use_alpha, stream);
+        return launch_tile<HEAL_MEDIUM_CFG>(a, trans_b, use_alpha, stream);
     case HEAL_INSTANCE_SKINNY:
-        if (a.M <= 16) return launch_tile<16, 64, 64, 16, 16, 256>(a, trans_b, use_alpha, stream);
-        if (a.M <= 32) return launch_tile<32, 64, 64, 32, 16, 256>(a, trans_b, use_alpha, stream);
-        return launch_tile<64, 64, 64, 64, 16, 256>(a, trans_b, use_alpha, stream);
+        if (skinny_kernel_applies(a, trans_b)) return launch_gemm_skinny(a, trans_b, use_alpha, stream);
+        if (a.M <= 16) return launch_tile<HEAL_SKINNY16_CFG>(a, trans_b, use_alpha, stream);
+        if (a.M <= 32) return launch_tile<HEAL_SKINNY32_CFG>(a, trans_b, use_alpha, stream);
+        return launch_tile<HEAL_SKINNY64_CFG>(a, trans_b, use_alpha, stream);
     default:
         return hipErrorInvalidValue;
     }

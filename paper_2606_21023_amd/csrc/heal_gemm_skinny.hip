@@ -1,0 +1,440 @@
+// The skinny compensated bf16x3 GEMM for gfx950 (MI355X): M <= 64 rows,
+// the decode and lm_head shapes, where the product is bound by streaming B
+// from HBM.
+//
+// HEAL Section 4 (GEMM paragraph and its displayed expansion): both FP32
+// operands are split into bf16 (hi, lo) and C = hiA*hiB + hiA*loB + loA*hiB,
+// summed in FP32 and written as FP32.
+//
+// Work split.  A workgroup owns a strip of BN = 16*CB columns of C and all
+// of its (at most 64) rows, and walks K in stages of BK.  Each element of B
+// is therefore loaded and split by exactly one workgroup; A (at most 64 x K,
+// resident in L2) is re-read by every workgroup.  Strips are narrow (16
+// columns for 4096-wide outputs) so that every CU streams its own share of
+// B: HBM bandwidth needs all CUs with loads in flight.
+//
+// Pipeline.  B is staged in a ring of R register sets: while stage s is
+// multiplied out of LDS, stage s+1 is split into the other LDS buffer and
+// its register set is reloaded with stage s+1+R, so each HBM load has R
+// stages to arrive.
+// A (L2 hits) is staged one stage ahead.  Split, LDS layout and fragment
+// reads follow the large kernel: 16-byte buffer loads, 4x4 register
+// transposes of B stored K x N, hi and lo planes with k-contiguous rows,
+// 16x16x32 bf16 MFMA fragments.  Lanes outside the matrix read zeros through
+// out-of-range buffer offsets; with K % BK != 0 the last stage is masked
+// along K the same way.
+//
+// Reduction order: identical to every other instance (K in 32-deep chunks
+// ascending, hiA*hiB, hiA*loB, loA*hiB into one FP32 accumulator, K tail
+// zero-filled, the B fragment as the MFMA's first source), so results are
+// bitwise equal to them.
+#include "heal.h"
+#include "heal_device.h"
+#include "heal_internal.h"
+
+namespace heal {
+
+namespace {
+
+constexpr int kNT = 256;
+constexpr uint32_t kOOB = 0x80000000u;  // buffer offset beyond every range: reads 0
+
+__device__ __forceinline__ f32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff)
+{
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, soff, 0));
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, int64_t bytes)
+{
+    // raw buffer, 32-bit elements; `bytes` < 2^31 is checked on the host
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+// LDS geometry of one stage for a given depth BK (bytes per plane row RP =
+// 2*BK).  The LDS has 64 four-byte banks (256-byte bank lines).
+//  * chunk swizzle: the 16-byte chunk c of row r is stored at c ^ swz(r),
+//    so the 16 lanes of a fragment read (16 rows, one chunk) hit 16
+//    different 16-byte bank slots;
+//  * brow: the LDS row of B column n (B stored K x N), chosen so that one
+//    transposed 8-byte store instruction (32 lanes per cycle) covers all
+//    banks; it permutes rows within aligned groups of 16, which fragment
+//    reads cover whole.
+template <int BK>
+struct Lds {
+    static constexpr int RP = 2 * BK;
+    static_assert(BK == 32 || BK == 64 || BK >= 128, "stage depth");
+    static __device__ __forceinline__ int swz(int row)
+    {
+        return RP >= 256 ? (row & 15) : RP == 128 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+    }
+    static __device__ __forceinline__ int brow(int n)
+    {
+        return RP >= 256 ? n : RP == 128 ? (n ^ ((n >> 2) & 1)) : (n ^ ((n >> 2) & 3));
+    }
+    static __device__ __forceinline__ int chunk_off(int row, int c)
+    {
+        return row * RP + ((c ^ swz(row)) << 4);
+    }
+    static __device__ __forceinline__ int quad_off(int row, int kq)
+    {
+        return row * RP + (((kq >> 1) ^ swz(row)) << 4) + ((kq & 1) << 3);
+    }
+};
+
+__device__ __forceinline__ void lds_store2(char *base, int off, uint32_t a, uint32_t b)
+{
+    u32x2 v = {a, b};
+    *reinterpret_cast<u32x2 *>(base + off) = v;
+}
+
+__device__ __forceinline__ bf16x8 lds_frag(const char *base, int off)
+{
+    return *reinterpret_cast<const bf16x8 *>(base + off);
+}
+
+// Workgroups per CU the LDS of one configuration allows (two when a
+// workgroup's two stage buffers fit in half of the 160 KB).
+constexpr int skinny_occupancy(int MB, int CB, int BK)
+{
+    return 2 * 2 * (16 * MB + 16 * CB) * (2 * BK) <= 80 * 1024 ? 2 : 1;
+}
+
+// MB: 16-row blocks of the tile (M <= 16*MB); CB: 16-column blocks per
+// workgroup; BK: stage depth.
+// R: depth of the B register ring (stages in flight from HBM), even.
+template <int MB, int CB, int BK, int R, bool TRANS_B, bool ALPHA, bool TAIL>
+__global__ void __launch_bounds__(kNT, skinny_occupancy(MB, CB, BK))
+gemm_skinny_kernel(GemmArgs p)
+{
+    static_assert(R >= 2 && R % 2 == 0, "ring depth");
+    using L = Lds<BK>;
+    constexpr int BM = 16 * MB, BN = 16 * CB, KQ = BK / 4, RP = L::RP;
+    constexpr int A_PLANE = BM * RP, B_PLANE = BN * RP;
+    constexpr int STAGE = 2 * A_PLANE + 2 * B_PLANE;
+    // per thread and stage: NA quads of A; NB quads of B (N x K) or NB/4
+    // 4x4 blocks of B (K x N)
+    constexpr int NA = BM * KQ / kNT;
+    constexpr int NB = BN * KQ / kNT;
+    static_assert(NA >= 1 && NA * kNT == BM * KQ, "A quads per thread");
+    static_assert(NB >= 1 && NB * kNT == BN * KQ, "B quads per thread");
+    static_assert(TRANS_B || NB % 4 == 0, "whole 4x4 B blocks per thread");
+    constexpr int CW = CB < 4 ? CB : 4;         // waves that multiply
+    constexpr int JW = CB / CW;                 // column blocks per computing wave
+    static_assert(CB % CW == 0, "column blocks per wave");
+
+    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int fr = lane & 15, fg = lane >> 4;
+
+    const int64_t n0 = (int64_t)blockIdx.x * BN;
+    const int64_t M = p.M, N = p.N, K = p.K;
+    const int cols = (int)((N - n0) < BN ? (N - n0) : BN);
+    const int ns = (int)((K + BK - 1) / BK);
+    const int k_end = (int)K;
+
+    // A quads: q = tid + 256u -> row q / KQ, k-quad q % KQ
+    int a_row[NA], a_kq[NA], st_a[NA];
+#pragma unroll
+    for (int u = 0; u < NA; ++u) {
+        const int q = tid + kNT * u;
+        a_row[u] = q / KQ;
+        a_kq[u] = q % KQ;
+        st_a[u] = L::quad_off(a_row[u], a_kq[u]);
+    }
+    // B: N x K quads (like A), or K x N 4x4 blocks b = tid + 256u with
+    // k-quad b % KQ and column group b / KQ
+    int b_kq[NB], b_n[NB], st_b[NB];
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+        if (TRANS_B) {
+            const int q = tid + kNT * u;
+            b_n[u] = q / KQ;
+            b_kq[u] = q % KQ;
+            st_b[u] = L::quad_off(b_n[u], b_kq[u]);
+        } else {
+            const int bl = tid + kNT * (u >> 2), nn = u & 3;
+            b_kq[u] = bl % KQ;
+            b_n[u] = 4 * (bl / KQ) + nn;              // column of unit u
+            st_b[u] = L::quad_off(L::brow(b_n[u]), b_kq[u]);
+        }
+    }
+    const int wj0 = wave;                        // first column block of this wave
+
+    for (int64_t b = blockIdx.y; b < p.batch; b += gridDim.y) {
+        const float *__restrict__ A = p.A + b * p.strideA;
+        const float *__restrict__ B = p.B + b * p.strideB + (TRANS_B ? n0 * p.ldb : n0);
+        float *__restrict__ C = p.C + b * p.strideC;
+
+        const __amdgpu_buffer_rsrc_t ra_src = make_rsrc(A, ((M - 1) * p.lda + K) * 4);
+        const __amdgpu_buffer_rsrc_t rb_src =
+            TRANS_B ? make_rsrc(B, ((int64_t)(cols - 1) * p.ldb + K) * 4)
+                    : make_rsrc(B, ((K - 1) * p.ldb + cols) * 4);
+        uint32_t va[NA], vb[NB];
+#pragma unroll
+        for (int u = 0; u < NA; ++u)
+            va[u] = a_row[u] < M ? (uint32_t)((a_row[u] * p.lda + 4 * a_kq[u]) * 4) : kOOB;
+#pragma unroll
+        for (int u = 0; u < NB; ++u) {
+            if (TRANS_B)
+                vb[u] = b_n[u] < cols ? (uint32_t)((b_n[u] * p.ldb + 4 * b_kq[u]) * 4) : kOOB;
+            else {
+                const int nq4 = b_n[u] & ~3;         // first column of the block
+                vb[u] = nq4 < cols ? (uint32_t)((4 * b_kq[u] * p.ldb + nq4) * 4) : kOOB;
+            }
+        }
+        const int ldb4 = (int)(p.ldb * 4);
+
+        f32x4 xa[NA];        // staged A (one stage)
+        f32x4 xb[R][NB];     // staged B (R stages, set = stage % R)
+
+        auto load_a = [&](int s) {
+#pragma unroll
+            for (int u = 0; u < NA; ++u) {
+                uint32_t v = va[u];
+                if (TAIL && s * BK + 4 * a_kq[u] >= k_end) v = kOOB;
+                xa[u] = bload(ra_src, v, s * BK * 4);
+            }
+        };
+        auto load_b = [&](int set, int s) {
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                uint32_t v = vb[u];
+                if (TRANS_B) {
+                    if (TAIL && s * BK + 4 * b_kq[u] >= k_end) v = kOOB;
+                    xb[set][u] = bload(rb_src, v, s * BK * 4);
+                } else {
+                    // row kk = u & 3 of block u >> 2
+                    const int kk = u & 3;
+                    if (TAIL && s * BK + 4 * b_kq[u] + kk >= k_end) v = kOOB;
+                    xb[set][u] = bload(rb_src, v, (s * BK + kk) * ldb4);
+                }
+            }
+        };
+        auto split_a = [&](char *st) {
+#pragma unroll
+            for (int u = 0; u < NA; ++u) {
+                uint32_t h0, l0, h1, l1;
+                split2(xa[u].x, xa[u].y, h0, l0);
+                split2(xa[u].z, xa[u].w, h1, l1);
+                lds_store2(st, st_a[u], h0, h1);
+                lds_store2(st + A_PLANE, st_a[u], l0, l1);
+            }
+        };
+        auto split_b = [&](char *st, int set) {
+            char *bh = st + 2 * A_PLANE, *bl = bh + B_PLANE;
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                uint32_t h0, l0, h1, l1;
+                if (TRANS_B) {
+                    split2(xb[set][u].x, xb[set][u].y, h0, l0);
+                    split2(xb[set][u].z, xb[set][u].w, h1, l1);
+                } else {
+                    // column nn of the block: element nn of its four rows
+                    const int blk = u >> 2, nn = u & 3;
+                    split2(xb[set][4 * blk + 0][nn], xb[set][4 * blk + 1][nn], h0, l0);
+                    split2(xb[set][4 * blk + 2][nn], xb[set][4 * blk + 3][nn], h1, l1);
+                }
+                lds_store2(bh, st_b[u], h0, h1);
+                lds_store2(bl, st_b[u], l0, l1);
+            }
+        };
+
+        f32x4 acc[MB][JW];
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int j = 0; j < JW; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+        // Multiply one stage out of the LDS buffer at `st`.  All fragment
+        // reads of the stage are issued first, in the order the MFMAs use
+        // them, so their latencies overlap instead of adding up per chunk.
+        auto compute = [&](const char *st) {
+            if (wave >= CW) return;
+            const char *ah = st, *al = st + A_PLANE;
+            const char *bh = st + 2 * A_PLANE, *bl = bh + B_PLANE;
+            constexpr int KC = BK / 32;
+            bf16x8 fah[KC][MB], fal[KC][MB], fbh[KC][JW], fbl[KC][JW];
+#pragma unroll
+            for (int kc = 0; kc < KC; ++kc) {
+#pragma unroll
+                for (int j = 0; j < JW; ++j) {
+                    const int col = (wj0 + CW * j) * 16 + fr;
+                    const int off = L::chunk_off(TRANS_B ? col : L::brow(col), 4 * kc + fg);
+                    fbh[kc][j] = lds_frag(bh, off);
+                    fbl[kc][j] = lds_frag(bl, off);
+                }
+#pragma unroll
+                for (int i = 0; i < MB; ++i) {
+                    const int off = L::chunk_off(i * 16 + fr, 4 * kc + fg);
+                    fah[kc][i] = lds_frag(ah, off);
+                    fal[kc][i] = lds_frag(al, off);
+                }
+            }
+#pragma unroll
+            for (int kc = 0; kc < KC; ++kc) {
+#pragma unroll
+                for (int j = 0; j < JW; ++j) {
+#pragma unroll
+                    for (int i = 0; i < MB; ++i)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fbh[kc][j], fah[kc][i], acc[i][j], 0, 0, 0);
+#pragma unroll
+                    for (int i = 0; i < MB; ++i)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fbl[kc][j], fah[kc][i], acc[i][j], 0, 0, 0);
+#pragma unroll
+                    for (int i = 0; i < MB; ++i)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fbh[kc][j], fal[kc][i], acc[i][j], 0, 0, 0);
+                }
+            }
+        };
+
+        const int last = ns - 1;
+        if (ns > 0) {
+            // prologue: stage 0 into buffer 0; A stage 1 and B stages 1..R staged
+            load_a(0);
+            load_b(0, 0);
+            split_a(smem);
+            split_b(smem, 0);
+            load_a(1 < last ? 1 : last);
+#pragma unroll
+            for (int t = 1; t <= R; ++t) load_b(t % R, t < last ? t : last);
+            __syncthreads();
+        }
+        // main loop, R stages per trip so that LDS buffers and register sets
+        // are compile-time choices.  Stage s is multiplied out of buffer s&1
+        // while stage s+1 (register set (s+1)%R) is split into the other
+        // buffer; that set is then reloaded with stage s+1+R, so each HBM
+        // load has R stages to arrive.  Reload stages are clamped to the last
+        // stage (redundant loads, never used).
+        for (int s0 = 0; s0 < ns; s0 += R) {
+#pragma unroll
+            for (int t = 0; t < R; ++t) {
+                const int s = s0 + t;
+                if (t == 0 || s < ns) {
+                    char *cur = smem + (t & 1) * STAGE;
+                    char *nxt = smem + ((t + 1) & 1) * STAGE;
+                    compute(cur);
+                    split_a(nxt);
+                    split_b(nxt, (t + 1) % R);
+                    load_a(s + 2 < last ? s + 2 : last);
+                    load_b((t + 1) % R, s + 1 + R < last ? s + 1 + R : last);
+                    __syncthreads();
+                }
+            }
+        }
+
+        // ---- epilogue: FP32 accumulators -> FP32 C, no downcast ----------
+        if (wave < CW) {
+#pragma unroll
+            for (int i = 0; i < MB; ++i) {
+                const int64_t m = i * 16 + fr;
+#pragma unroll
+                for (int j = 0; j < JW; ++j) {
+                    const int64_t n = n0 + (wj0 + CW * j) * 16 + 4 * fg;
+                    f32x4 v = acc[i][j];
+                    if (ALPHA) v = v * p.alpha;
+                    if (m < M && n < N) *reinterpret_cast<f32x4 *>(C + m * p.ldc + n) = v;
+                }
+            }
+        }
+    }
+}
+
+template <int MB, int CB, int BK, int R, bool TRANS_B, bool ALPHA>
+hipError_t launch(const GemmArgs &a, hipStream_t stream)
+{
+    const int64_t tiles = (a.N + 16 * CB - 1) / (16 * CB);
+    const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
+    if (a.K % BK)
+        hipLaunchKernelGGL((gemm_skinny_kernel<MB, CB, BK, R, TRANS_B, ALPHA, true>),
+                           dim3((unsigned)tiles, gy), dim3(kNT), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm_skinny_kernel<MB, CB, BK, R, TRANS_B, ALPHA, false>),
+                           dim3((unsigned)tiles, gy), dim3(kNT), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int MB, int CB, int BK, int R>
+hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
+{
+    if (trans_b)
+        return use_alpha ? launch<MB, CB, BK, R, true, true>(a, stream)
+                         : launch<MB, CB, BK, R, true, false>(a, stream);
+    return use_alpha ? launch<MB, CB, BK, R, false, true>(a, stream)
+                     : launch<MB, CB, BK, R, false, false>(a, stream);
+}
+
+// Strip width, stage depth and B ring depth by shape.  Measured on the
+// MI355X with a read-only kernel of the same access pattern (4096-deep B):
+// 16-column strips read 64-byte pieces of rows that lie a full row pitch
+// apart and stream at ~2.7 TB/s, 32-column strips at ~5.5 TB/s, 128- and
+// 256-column strips at ~6.8 TB/s when there are enough of them.  Outputs
+// of 4096 columns have only 256 16-column strips, one per CU, which still
+// beats 128 wider ones; wide outputs (lm_head) use 256-column strips.  The
+// stage depth is the smallest that gives every thread whole 16-byte units
+// of A and B at the tile's row count.
+#ifndef HEAL_SKINNY_N1
+#define HEAL_SKINNY_N1 1, 256, 2      // M <= 16, narrow: CB, BK, R
+#endif
+#ifndef HEAL_SKINNY_N2
+#define HEAL_SKINNY_N2 2, 256, 2
+#endif
+#ifndef HEAL_SKINNY_N4
+#define HEAL_SKINNY_N4 2, 128, 2
+#endif
+#ifndef HEAL_SKINNY_W1
+#define HEAL_SKINNY_W1 8, 128, 2      // M <= 16, wide (strips of 16*CB columns)
+#endif
+#ifndef HEAL_SKINNY_W2
+#define HEAL_SKINNY_W2 8, 64, 2
+#endif
+#ifndef HEAL_SKINNY_W4
+#define HEAL_SKINNY_W4 16, 32, 2
+#endif
+#ifndef HEAL_SKINNY_WIDE_MIN_N
+#define HEAL_SKINNY_WIDE_MIN_N 16384
+#endif
+
+template <int MB>
+hipError_t launch_shape(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
+{
+    const bool wide = a.N >= HEAL_SKINNY_WIDE_MIN_N;
+    if constexpr (MB == 1)
+        return wide ? launch_mb<1, HEAL_SKINNY_W1>(a, trans_b, use_alpha, stream)
+                    : launch_mb<1, HEAL_SKINNY_N1>(a, trans_b, use_alpha, stream);
+    else if constexpr (MB == 2)
+        return wide ? launch_mb<2, HEAL_SKINNY_W2>(a, trans_b, use_alpha, stream)
+                    : launch_mb<2, HEAL_SKINNY_N2>(a, trans_b, use_alpha, stream);
+    else
+        return wide ? launch_mb<4, HEAL_SKINNY_W4>(a, trans_b, use_alpha, stream)
+                    : launch_mb<4, HEAL_SKINNY_N4>(a, trans_b, use_alpha, stream);
+}
+
+}  // namespace
+
+bool skinny_kernel_applies(const GemmArgs &a, bool trans_b)
+{
+    // At most 64 rows, 16-byte rows, whole quads along K (and N).  Buffer
+    // offsets are 32-bit: the largest is that of the last element a lane may
+    // address, (M-1)*lda + K (+ one 256-deep stage for a clamped reload) for
+    // A, the same with the 256-row strip for B stored N x K, and
+    // (K+3)*ldb + 256 for B stored K x N (row k + kk of a 4-row block).
+    if (a.M > 64 || !(a.vecA && a.vecB && a.vecC) || a.K % 4 != 0 || a.N % 4 != 0) return false;
+    const int64_t lim = 0x7fffffffLL;
+    if (((a.M - 1) * a.lda + a.K + 256) * 4 >= lim) return false;
+    if (trans_b ? ((int64_t)255 * a.ldb + a.K + 256) * 4 >= lim : ((a.K + 3) * a.ldb + 256) * 4 >= lim)
+        return false;
+    return (a.N + 15) / 16 <= 0x7fffffffLL;
+}
+
+hipError_t launch_gemm_skinny(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
+{
+    if (a.M <= 16) return launch_shape<1>(a, trans_b, use_alpha, stream);
+    if (a.M <= 32) return launch_shape<2>(a, trans_b, use_alpha, stream);
+    return launch_shape<4>(a, trans_b, use_alpha, stream);
+}
+
+}  // namespace heal

@@ -33,6 +33,11 @@ bool large_kernel_applies(const GemmArgs &args, bool trans_b);
 hipError_t launch_gemm_large(const GemmArgs &args, bool trans_b, bool use_alpha,
                              hipStream_t stream);
 
+// The skinny kernel (heal_gemm_skinny.hip): M <= 64, 16-byte operand rows.
+bool skinny_kernel_applies(const GemmArgs &args, bool trans_b);
+hipError_t launch_gemm_skinny(const GemmArgs &args, bool trans_b, bool use_alpha,
+                              hipStream_t stream);
+
 hipError_t launch_split(const float *x, uint16_t *hi, uint16_t *lo, int64_t n, hipStream_t stream);
 
 }  // namespace heal
