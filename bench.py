@@ -43,12 +43,14 @@ sys.path.insert(0, ROOT)
 BF16_DENSE_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 bf16 flop/clk/CU (MI355X, dense)
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = ["heal_gemm.hip", "heal_gemm_large.hip", "heal_gemm_skinny.hip", "heal_device.h",
-                  "heal_internal.h"]
-# the kernel each instance of heal_gemm_f32 launches (16-byte aligned operands)
-KERNEL_NAMES = {1: "gemm_large_kernel (256x256 tiles, 4 waves)",
+# the kernel each instance of heal_gemm_f32 launches (16-byte aligned
+# operands), and the sources that define it
+KERNEL_NAMES = {1: "gemm_large8_kernel (256x256 tiles, 8 waves of 64x128)",
                 2: "gemm_bf16x3_kernel<128,128,32,64,64,256> (medium)",
                 3: "gemm_skinny_kernel (column strips, M <= 64)"}
+KERNEL_SOURCES = {1: ["heal_gemm_large.hip", "heal_device.h", "heal_internal.h"],
+                  2: ["heal_gemm.hip", "heal_device.h", "heal_internal.h"],
+                  3: ["heal_gemm_skinny.hip", "heal_device.h", "heal_internal.h"]}
 
 
 def parse():
@@ -66,22 +68,23 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_source_hash():
+def kernel_source_hash(instance):
+    """Hash of the sources of the kernel an instance launches."""
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in KERNEL_SOURCES[instance]:
         with open(os.path.join(ROOT, "paper_2606_21023_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload):
+def measured_traffic(workload, instance):
     """HBM bytes per launch from counters, if measured on the current kernel sources."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     with open(TRAFFIC_FILE) as f:
         t = json.load(f)
     e = t.get("workloads", {}).get(workload)
-    if not e or t.get("kernel_source_sha") != kernel_source_hash():
+    if not e or e.get("kernel_source_sha") != kernel_source_hash(instance):
         return None
     return e["fetch_kib"] * 1024.0 * t["read_factor"] + e["write_kib"] * 1024.0 * t["write_factor"]
 
@@ -188,7 +191,8 @@ def main():
     mfma_flops = 3.0 * flops
     t_mfma = mfma_flops / (BF16_DENSE_PEAK_TFLOPS * 1e12)
     t_hbm = w.algorithmic_bytes / (HBM_PEAK_GBS * 1e9)
-    traffic = measured_traffic(w.name)
+    instance = heal.select_instance(w.M, w.N)
+    traffic = measured_traffic(w.name, instance)
     if t_mfma >= t_hbm:
         achieved = mfma_flops / (avg_launch_ms * 1e-3) / 1e12
         roofline = {"bound": "mfma", "achieved": round(achieved, 2),
@@ -201,7 +205,7 @@ def main():
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
         per_launch = "4*(M*K + K*N + M*N)*batch bytes = %.4g" % w.algorithmic_bytes
     roofline.update({"traffic": None if traffic is None else round(traffic),
-                     "kernel": KERNEL_NAMES.get(heal.select_instance(w.M, w.N), "?"),
+                     "kernel": KERNEL_NAMES.get(instance, "?"),
                      "per_launch": per_launch, "avg_launch_us": round(avg_launch_ms * 1e3, 2)})
 
     # MI355X native FP32 GEMM on the same inputs, TF32 off

@@ -1,20 +1,25 @@
 // The large-tile compensated bf16x3 GEMM for gfx950 (MI355X): 256 x 256
-// output tiles, four waves of 128 x 128, one wave per SIMD.
+// output tiles.  Two forms share the data path below: eight waves of
+// 64 x 128 (two waves per SIMD, the default) and four waves of 128 x 128
+// (one wave per SIMD).
 //
 // HEAL Section 4 (GEMM paragraph and its displayed expansion) keeps a GEMM
 // on the 16-bit matrix units and recovers the bits a single 16-bit cast
 // drops by adding residual products, summed in FP32.  Both FP32 operands are
 // split into bf16 (hi, lo) and C = hiA*hiB + hiA*loB + loA*hiB.
 //
-// Why this shape.  Per 32-deep stage the workgroup moves 64 KB of FP32 from
-// L2, splits it (six VALU instructions per element pair), stores 64 KB of
-// bf16 planes into LDS and reads 128 KB of MFMA fragments back, against 768
-// bf16 MFMAs (3072 cycles per SIMD).  Wave tiles of 128 x 128 read a third
-// fewer LDS bytes per MFMA than 64 x 128 tiles; with one wave per SIMD each
-// wave has the whole 512-entry register file, so its 256 FP32 accumulators
-// live in AGPRs and the fragments, the staged FP32 data and the split fit in
-// VGPRs.  The split and the LDS traffic are interleaved with the MFMAs of
-// the same wave.
+// Why these shapes.  Per 32-deep stage the workgroup moves 64 KB of FP32
+// from L2, splits it (six VALU instructions per element pair), stores 64 KB
+// of bf16 planes into LDS and reads the MFMA fragments back, against 768
+// bf16 MFMAs.  On gfx950 one wave cannot issue 16x16x32 bf16 MFMAs back to
+// back: a register-only loop sustains about two thirds of the matrix core's
+// rate with one wave per SIMD and nearly all of it with two.  The eight-wave
+// form therefore keeps two waves per SIMD (128 accumulators each, 64 x 128
+// wave tiles, 192 KB of fragment reads per stage); the four-wave form reads
+// a third less LDS (128 x 128 wave tiles, 256 accumulators per lane in
+// AGPRs) but is capped by the single-wave issue rate.  On 8192^3 the
+// eight-wave form is about 4% faster, on 2048 x 14336 x 4096 about 11%.
+// In both, the split and the LDS traffic are interleaved with the MFMAs.
 //
 // Pipeline.  Two LDS stage buffers.  While stage s is multiplied out of one
 // buffer, the FP32 data of stage s+1 (already in VGPRs) is split into the
@@ -48,6 +53,12 @@ constexpr int kStage = 4 * kPlane;      // A_hi, A_lo, B_hi, B_lo
 constexpr uint32_t kOOB = 0x80000000u;  // buffer offset beyond every range: reads 0
 
 // Instruction interleave of one 24-MFMA group (tuning knobs).
+#ifndef HEAL_LARGE_WAVES
+#define HEAL_LARGE_WAVES 8
+#endif
+#ifndef HEAL_L8_PATTERN
+#define HEAL_L8_PATTERN 1
+#endif
 #ifndef HEAL_LARGE_VALU_SLOTS
 #define HEAL_LARGE_VALU_SLOTS 12
 #endif
@@ -335,17 +346,243 @@ gemm_large_kernel(GemmArgs p)
     }
 }
 
+
+// Eight-wave form: two waves per SIMD, wave tiles of 64 x 128 (128 FP32
+// accumulators per lane).  A single wave cannot issue 16x16x32 MFMAs back to
+// back (it sustains about two thirds of the matrix core's rate); two waves
+// per SIMD can.  Same LDS layout, loads, split and per-element order as the
+// four-wave form; the MFMA loop walks the eight 16-column blocks of the wave
+// tile with the four A fragment pairs resident.
+template <bool TRANS_B, bool ALPHA, bool TAIL>
+__global__ void __launch_bounds__(512, 1)
+gemm_large8_kernel(GemmArgs p)
+{
+    constexpr int NT = 512;
+    // Thread -> data maps (per stage, 8 loads of 16 bytes per thread):
+    //   A, and B stored N x K: quad u (0..3) is row tid/8 + 64u, k-quad tid%8.
+    //   B stored K x N: the 4 (k) x 4 (n) block with k-quad (lane>>1)&7 and
+    //     column group (lane&1) | (lane>>4)<<1 | wave<<3.
+    __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave & 3, wn = wave >> 2;
+    const int fr = lane & 15, fg = lane >> 4;
+
+    const int64_t tiles_m = (p.M + kBM - 1) / kBM;
+    const int64_t tiles_n = (p.N + kBN - 1) / kBN;
+    const int64_t nb = (int64_t)gridDim.x;
+    int64_t bid = blockIdx.x;
+    {
+        const int64_t x = bid & 7, i = bid >> 3, q = nb >> 3, r = nb & 7;
+        bid = x * q + (x < r ? x : r) + i;
+    }
+    constexpr int GM = HEAL_GROUP_M;
+    const int64_t group = bid / (GM * tiles_n);
+    const int64_t first_m = group * GM;
+    const int64_t gm = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
+    const int64_t in_group = bid - group * GM * tiles_n;
+    const int64_t m0 = (first_m + in_group % gm) * kBM;
+    const int64_t n0 = (in_group / gm) * kBN;
+
+    const int64_t M = p.M, N = p.N, K = p.K;
+    const int rows_a = (int)((M - m0) < kBM ? (M - m0) : kBM);
+    const int cols_b = (int)((N - n0) < kBN ? (N - n0) : kBN);
+    const int ns = (int)((K + kBK - 1) / kBK);
+
+    const int a_row = tid >> 3, a_kq = tid & 7;
+    const int b_kq = (lane >> 1) & 7;
+    const int b_nq = (lane & 1) | ((lane >> 4) << 1) | (wave << 3);
+    const int st_a = quad_off(a_row, a_kq);
+    int st_b[4];
+#pragma unroll
+    for (int nn = 0; nn < 4; ++nn) st_b[nn] = TRANS_B ? st_a : quad_off(brow(4 * b_nq + nn), b_kq);
+    const int rd_a = chunk_off(wm * 64 + fr, fg);
+    const int rd_b = chunk_off(TRANS_B ? wn * kWT + fr : brow(wn * kWT + fr), fg);
+
+    for (int64_t b = blockIdx.y; b < p.batch; b += gridDim.y) {
+        const float *__restrict__ A = p.A + b * p.strideA + m0 * p.lda;
+        const float *__restrict__ B = p.B + b * p.strideB + (TRANS_B ? n0 * p.ldb : n0);
+        float *__restrict__ C = p.C + b * p.strideC;
+
+        const __amdgpu_buffer_rsrc_t ra_src = make_rsrc(A, ((int64_t)(rows_a - 1) * p.lda + K) * 4);
+        const __amdgpu_buffer_rsrc_t rb_src =
+            TRANS_B ? make_rsrc(B, ((int64_t)(cols_b - 1) * p.ldb + K) * 4)
+                    : make_rsrc(B, ((K - 1) * p.ldb + cols_b) * 4);
+        uint32_t va[4], vb[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            va[u] = a_row + 64 * u < rows_a ? (uint32_t)(((a_row + 64 * u) * p.lda + 4 * a_kq) * 4) : kOOB;
+        if (TRANS_B) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                vb[u] = a_row + 64 * u < cols_b ? (uint32_t)(((a_row + 64 * u) * p.ldb + 4 * a_kq) * 4) : kOOB;
+        } else {
+            const int n = 4 * b_nq;
+            vb[0] = n < cols_b ? (uint32_t)((4 * b_kq * p.ldb + n) * 4) : kOOB;
+        }
+        const int ldb4 = (int)(p.ldb * 4);
+        const int k_end = (int)K;
+
+        f32x4 ra[4], rb[4];
+        auto load_a = [&](int u, int s) {
+            uint32_t v = va[u];
+            if (TAIL && s * kBK + 4 * a_kq >= k_end) v = kOOB;
+            ra[u] = bload(ra_src, v, s * kBK * 4);
+        };
+        auto load_b = [&](int u, int s) {
+            if (TRANS_B) {
+                uint32_t v = vb[u];
+                if (TAIL && s * kBK + 4 * a_kq >= k_end) v = kOOB;
+                rb[u] = bload(rb_src, v, s * kBK * 4);
+            } else {
+                const int kk = u;            // row kk of the block
+                uint32_t v = vb[0];
+                if (TAIL && s * kBK + 4 * b_kq + kk >= k_end) v = kOOB;
+                rb[u] = bload(rb_src, v, (s * kBK + kk) * ldb4);
+            }
+        };
+        auto split_unit = [&](char *s, int u) {
+            uint32_t h0, l0, h1, l1;
+            if (u < 4) {
+                split2(ra[u].x, ra[u].y, h0, l0);
+                split2(ra[u].z, ra[u].w, h1, l1);
+                lds_store2(s, st_a + u * 64 * kRowB, h0, h1);
+                lds_store2(s + kPlane, st_a + u * 64 * kRowB, l0, l1);
+            } else if (TRANS_B) {
+                const int v = u - 4;
+                split2(rb[v].x, rb[v].y, h0, l0);
+                split2(rb[v].z, rb[v].w, h1, l1);
+                lds_store2(s + 2 * kPlane, st_a + v * 64 * kRowB, h0, h1);
+                lds_store2(s + 3 * kPlane, st_a + v * 64 * kRowB, l0, l1);
+            } else {
+                const int nn = u - 4;
+                split2(rb[0][nn], rb[1][nn], h0, l0);
+                split2(rb[2][nn], rb[3][nn], h1, l1);
+                lds_store2(s + 2 * kPlane, st_b[nn], h0, h1);
+                lds_store2(s + 3 * kPlane, st_b[nn], l0, l1);
+            }
+        };
+        auto reload_unit = [&](int u, int s) {
+            if (u < 4) {
+                load_a(u, s);
+            } else if (TRANS_B) {
+                load_b(u - 4, s);
+            } else if (u == 7) {
+#pragma unroll
+                for (int kk = 0; kk < 4; ++kk) load_b(kk, s);
+            }
+        };
+
+        f32x4 acc[8][4];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+        if (ns > 0) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) load_a(u, 0);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) load_b(u, 0);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) split_unit(smem, u);
+            const int s1 = ns > 1 ? 1 : 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) load_a(u, s1);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) load_b(u, s1);
+            __syncthreads();
+        }
+
+        for (int s = 0; s < ns; ++s) {
+            const char *cur = smem + (s & 1) * kStage;
+            char *nxt = smem + ((s + 1) & 1) * kStage;
+            const int s_reload = s + 2 < ns ? s + 2 : ns - 1;
+            const char *a_hi = cur, *a_lo = cur + kPlane;
+            const char *b_hi = cur + 2 * kPlane, *b_lo = cur + 3 * kPlane;
+            bf16x8 ah[4], al[4], bh[2], bl[2];
+            bh[0] = lds_frag(b_hi, rd_b);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ah[i] = lds_frag(a_hi, rd_a + i * 16 * kRowB);
+            bl[0] = lds_frag(b_lo, rd_b);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) al[i] = lds_frag(a_lo, rd_a + i * 16 * kRowB);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int c = j & 1;
+                if (j + 1 < 8) {
+                    bh[c ^ 1] = lds_frag(b_hi, rd_b + (j + 1) * 16 * kRowB);
+                    bl[c ^ 1] = lds_frag(b_lo, rd_b + (j + 1) * 16 * kRowB);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[c], ah[i], acc[j][i], 0, 0, 0);
+                split_unit(nxt, j);
+                reload_unit(j, s_reload);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bl[c], ah[i], acc[j][i], 0, 0, 0);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[c], al[i], acc[j][i], 0, 0, 0);
+#if HEAL_L8_PATTERN == 1
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+                for (int t = 0; t < 6; ++t) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+#elif HEAL_L8_PATTERN == 2
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+                for (int t = 0; t < 12; ++t) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+#endif
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __syncthreads();
+        }
+
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t m = m0 + wm * 64 + i * 16 + fr;
+                const int64_t n = n0 + wn * kWT + j * 16 + 4 * fg;
+                f32x4 v = acc[j][i];
+                if (ALPHA) v = v * p.alpha;
+                if (m < M && n < N) *reinterpret_cast<f32x4 *>(C + m * p.ldc + n) = v;
+            }
+        }
+    }
+}
+
 template <bool TRANS_B, bool ALPHA>
 hipError_t launch(const GemmArgs &a, hipStream_t stream)
 {
     const int64_t tiles = ((a.M + kBM - 1) / kBM) * ((a.N + kBN - 1) / kBN);
     const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
+    const dim3 grid((unsigned)tiles, gy);
+#if HEAL_LARGE_WAVES == 8
     if (a.K % kBK)
-        hipLaunchKernelGGL((gemm_large_kernel<TRANS_B, ALPHA, true>), dim3((unsigned)tiles, gy),
-                           dim3(kNT), 0, stream, a);
+        hipLaunchKernelGGL((gemm_large8_kernel<TRANS_B, ALPHA, true>), grid, dim3(512), 0, stream, a);
     else
-        hipLaunchKernelGGL((gemm_large_kernel<TRANS_B, ALPHA, false>), dim3((unsigned)tiles, gy),
-                           dim3(kNT), 0, stream, a);
+        hipLaunchKernelGGL((gemm_large8_kernel<TRANS_B, ALPHA, false>), grid, dim3(512), 0, stream, a);
+#else
+    if (a.K % kBK)
+        hipLaunchKernelGGL((gemm_large_kernel<TRANS_B, ALPHA, true>), grid, dim3(kNT), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm_large_kernel<TRANS_B, ALPHA, false>), grid, dim3(kNT), 0, stream, a);
+#endif
     return hipGetLastError();
 }
 
