@@ -12,6 +12,13 @@ mismatch.  They never compare the oracle with itself or with the HIP path:
   give the exact integer GEMM;
 * a brute-force error bound against the exact rational product on tiny sizes.
 
+The FP16 forms (HEAL-Base, HEAL-Full) and the INT16 score product (HEAL+)
+have pins of the same kinds: binary16 rounding against numpy's float16 casts,
+hand-derived golden pairs, the defining property of the weight exponent,
+closed-form error bounds against exact rational products, integer inputs, the
+exact identity hi + lo/2^10 = q of the INT16 unpack, and the paper's INT16
+error and MSE bounds.
+
 The mutation tests run the same pins against oracles with planted mistakes.
 """
 import os
@@ -356,6 +363,348 @@ def pin_nonfinite_propagation(orc):
     assert np.array_equal(C[2], np.array([5.0, -1.0], np.float32))
 
 
+# --------------------------------------------------------------------------
+# FP16 forms: binary16 rounding, the HEAL-Full pair, weight scaling, GEMM
+# --------------------------------------------------------------------------
+
+def _f16_to_f64(h):
+    return np.asarray(h, np.uint16).view(np.float16).astype(np.float64)
+
+
+def _nanh(h):
+    return np.isnan(np.asarray(h, np.uint16).view(np.float16))
+
+
+def _check_pairs_equal(x, hi, lo, hi_ref, lo_ref, what):
+    """Bitwise equality of binary16 pairs; NaNs compared by NaN-ness only."""
+    for name, a, b in (("hi", hi, hi_ref), ("lo", lo, lo_ref)):
+        if not np.array_equal(_nanh(a), _nanh(b)):
+            i = np.nonzero(_nanh(a) != _nanh(b))[0][0]
+            raise AssertionError("%s: NaN-ness of %s differs at x=%r" % (what, name, x[i]))
+    ok = ~(_nanh(hi_ref) | _nanh(lo_ref))
+    bad = np.nonzero((hi[ok] != hi_ref[ok]) | (lo[ok] != lo_ref[ok]))[0]
+    if bad.size:
+        i = np.nonzero(ok)[0][bad[0]]
+        raise AssertionError("%s: mismatch at x=%r: got (%04x,%04x), expected (%04x,%04x)"
+                             % (what, x[i], hi[i], lo[i], hi_ref[i], lo_ref[i]))
+
+
+def f16_boundary_doubles():
+    """Doubles at, next to and halfway between every pair of adjacent binary16
+    values (both signs), plus the overflow tie 65520 and its neighbours."""
+    h = np.arange(0, 0x7c00, dtype=np.uint16)              # +0 .. 65504
+    v = h.view(np.float16).astype(np.float64)
+    nxt = np.append(v[1:], 65536.0)                        # next value up (65536 past the end)
+    mid = (v + nxt) / 2.0                                  # exact in FP64
+    pts = np.concatenate([v, mid, np.nextafter(mid, 0.0), np.nextafter(mid, np.inf),
+                          np.nextafter(v, np.inf), [65520.0, np.nextafter(65520.0, 0.0),
+                                                    1e6, np.inf]])
+    return np.concatenate([pts, -pts, [np.nan]])
+
+
+def pin_f16_rne_vs_library(orc):
+    """binary16 rounding of doubles equals numpy's float64 -> float16 cast at
+    every value, tie and near-tie of the format, and on FP32 inputs of every
+    rounding class."""
+    x = f16_boundary_doubles()
+    got = orc.f16_rne(x)
+    with np.errstate(over="ignore"):
+        ref = x.astype(np.float16).view(np.uint16)
+    both_nan = _nanh(got) & _nanh(ref)
+    bad = np.nonzero((got != ref) & ~both_nan)[0]
+    assert bad.size == 0, "f16 RNE of %r: got %04x, numpy %04x" % (x[bad[0]], got[bad[0]],
+                                                                     ref[bad[0]])
+    xf = _f32_from_bits(structured_patterns())
+    with np.errstate(over="ignore", invalid="ignore"):
+        got = orc.f16_rne(xf.astype(np.float64))
+        ref = xf.astype(np.float16).view(np.uint16)
+    both_nan = _nanh(got) & _nanh(ref)
+    bad = np.nonzero((got != ref) & ~both_nan)[0]
+    assert bad.size == 0, "f16 RNE of FP32 %r: got %04x, numpy %04x" % (xf[bad[0]], got[bad[0]],
+                                                                         ref[bad[0]])
+
+
+def load_pair_golden(name):
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if line:
+                x, h, l = line.split()
+                rows.append((int(x, 16), None if h == "nan" else int(h, 16),
+                             None if l == "nan" else int(l, 16)))
+    return rows
+
+
+def pin_golden_split_f16(orc):
+    """Hand-derived HEAL-Full pairs; "nan" accepts any NaN pattern."""
+    rows = load_pair_golden("split_f16_cases.txt")
+    x = _f32_from_bits(np.array([r[0] for r in rows], np.uint32))
+    hi, lo = orc.split_f16(x)
+    for (xb, hb, lb), h, l in zip(rows, hi, lo):
+        for exp, got, name in ((hb, int(h), "hi"), (lb, int(l), "lo")):
+            if exp is None:
+                assert _nanh(np.uint16(got)), "golden f16 pair x=0x%08x: %s=%04x is not NaN" % (
+                    xb, name, got)
+            else:
+                assert got == exp, "golden f16 pair x=0x%08x: %s=%04x, expected %04x" % (
+                    xb, name, got, exp)
+
+
+def reference_split_f16(x):
+    """The HEAL-Full pair evaluated with library primitives: numpy's
+    float32 -> float16 cast for the head, FP64 for the shifted residual (exact)
+    and numpy's float64 -> float16 cast for it."""
+    x = np.ascontiguousarray(x, np.float32)
+    with np.errstate(over="ignore", invalid="ignore"):
+        hi = x.astype(np.float16)
+        r = (x.astype(np.float64) - hi.astype(np.float64)) * 1024.0
+        lo = r.astype(np.float16)
+    return hi.view(np.uint16), lo.view(np.uint16)
+
+
+def pin_split_f16_vs_library(orc):
+    x = _f32_from_bits(structured_patterns())
+    hi, lo = orc.split_f16(x)
+    hr, lr = reference_split_f16(x)
+    _check_pairs_equal(x, hi, lo, hr, lr, "f16 pair vs library")
+
+
+def check_split_f16_range_exhaustive(orc, start, n):
+    """Exhaustive form of pin_split_f16_vs_library over FP32 bit patterns
+    [start, start+n), the reference evaluated with torch CPU casts (the same
+    definition, multi-threaded)."""
+    hi, lo = orc.split_f16_range(start, n)
+    bits = torch.arange(n, dtype=torch.int64).add_(start).to(torch.int32)
+    x = bits.view(torch.float32)
+    hr = x.to(torch.float16)
+    lr = ((x.to(torch.float64) - hr.to(torch.float64)) * 1024.0).to(torch.float16)
+    hi_t = torch.from_numpy(hi.view(np.int16)).view(torch.float16)
+    lo_t = torch.from_numpy(lo.view(np.int16)).view(torch.float16)
+    what = "exhaustive f16 pair [0x%08x,+%d)" % (start, n)
+    hrn, lrn = torch.isnan(hr), torch.isnan(lr)
+    assert torch.equal(torch.isnan(hi_t), hrn), "%s: NaN-ness of hi differs" % what
+    assert torch.equal(torch.isnan(lo_t), lrn), "%s: NaN-ness of lo differs" % what
+    bad = ~(hrn | lrn) & ((hi_t.view(torch.int16) != hr.view(torch.int16)) |
+                          (lo_t.view(torch.int16) != lr.view(torch.int16)))
+    if torch.any(bad):
+        i = int(torch.nonzero(bad)[0, 0])
+        raise AssertionError("%s: mismatch at x=0x%08x" % (what, (start + i) & 0xffffffff))
+
+
+def pin_split_f16_properties(orc, seed=7):
+    """Properties of the HEAL-Full pair for finite inputs below the FP16 overflow.
+
+    * x - hi is exact in FP32 (so a device may evaluate it in FP32);
+    * |x - hi - 2^-10 lo| <= 2^-22 |x| + 2^-35: hi keeps 11 significant bits,
+      |x - hi| is at most half a step of hi (2^-11 relative), and lo rounds
+      2^10 (x - hi) to 11 more bits (or to the 2^-24 subnormal step);
+    * FP16-representable x gives hi = x and lo = 0.
+    """
+    rng = np.random.default_rng(seed)
+    n = 200000
+    e = rng.integers(-40, 16, size=n)
+    m = rng.random(n) + 1.0
+    x = (np.where(rng.random(n) < 0.5, -1.0, 1.0) * m * np.exp2(e)).astype(np.float32)
+    x = x[np.abs(x) < 65504.0]
+    hi, lo = orc.split_f16(x)
+    hf, lf = _f16_to_f64(hi), _f16_to_f64(lo)
+    x64 = x.astype(np.float64)
+    assert np.all(np.isfinite(hf)) and np.all(np.isfinite(lf)), "pair overflowed in range"
+    r32 = (x - hf.astype(np.float32)).astype(np.float64)
+    assert np.array_equal(r32, x64 - hf), "x - hi is not exact in FP32"
+    err = np.abs(x64 - hf - lf / 1024.0)
+    bound = np.ldexp(np.abs(x64), -22) + 2.0 ** -35
+    assert np.all(err <= bound), "pair error exceeds 2^-22|x| + 2^-35 (max ratio %g)" % np.max(
+        err / bound)
+    hb, lb = orc.split_f16(hf.astype(np.float32))
+    assert np.array_equal(hb, hi) and np.all(lb == 0), "pair of an FP16 value is not (x, 0)"
+
+
+def pin_weight_exponent(orc, seed=8):
+    """The weight exponent: golden values and its defining property
+    maxabs * 2^e <= 65504 < maxabs * 2^(e+1), checked in exact rationals."""
+    golden = [(1.0, 15), (65504.0, 0), (65505.0, -1), (0.0, 0), (0.01, 22), (2.0 ** -20, 35),
+              (32752.0, 1), (32753.0, 0), (3.0e38, -112), (2.0 ** -149, 164)]
+    for m, e in golden:
+        got = orc.f16_weight_exponent(float(np.float32(m)))
+        assert got == e, "weight exponent of %r: %d, expected %d" % (m, got, e)
+    rng = np.random.default_rng(seed)
+    ms = (np.exp2(rng.uniform(-140, 127, size=300)) * rng.uniform(1, 2, size=300)).astype(
+        np.float32)
+    top = Fraction(65504)
+    for m in ms:
+        if not np.isfinite(m) or m == 0:
+            continue
+        e = orc.f16_weight_exponent(float(m))
+        fm = Fraction(float(m))
+        assert fm * Fraction(2) ** e <= top < fm * Fraction(2) ** (e + 1), \
+            "weight exponent %d of %r violates its definition" % (e, m)
+
+
+def pin_f16_weights_vs_library(orc, seed=9):
+    """RNE_f16(W * 2^e) equals numpy's float64 -> float16 cast of the exactly
+    scaled weight, including weights that land in the FP16 subnormal range."""
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((37, 53)) * np.exp2(rng.integers(-30, 2, size=(37, 53)))).astype(
+        np.float32)
+    W[0, 0] = 0.0
+    W[1, 1] = -0.0
+    e = orc.f16_weight_exponent(float(np.abs(W).max()))
+    got = orc.f16_weights(W, e)
+    ref = np.ldexp(W.astype(np.float64), e).astype(np.float16).view(np.uint16)
+    assert np.array_equal(got, ref), "f16 weights differ from the library cast"
+    assert np.all(np.isfinite(_f16_to_f64(got))), "a scaled weight overflowed"
+
+
+def pin_gemm_f16w_integer(orc, seed=10):
+    """Integer activations |a| <= 2^11 are FP16-exact (lo = 0), integer weights
+    |w| <= 32 scale exactly (e = 10): S is the exact integer GEMM for both
+    forms, and C its FP32 rounding."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 11, 13, 45
+    A = rng.integers(-2048, 2049, size=(M, K)).astype(np.float32)
+    W = rng.integers(-32, 33, size=(N, K)).astype(np.float32)
+    W[0, 0] = 32.0
+    e = orc.f16_weight_exponent(float(np.abs(W).max()))
+    assert e == 10
+    ref = A.astype(np.int64) @ W.astype(np.int64).T
+    for products in (1, 2):
+        C, S = orc.gemm_f16w(A, W, e, products)
+        assert np.array_equal(S, ref.astype(np.float64)), "integer f16 GEMM: S != exact"
+        assert np.array_equal(C, ref.astype(np.float32)), "integer f16 GEMM: C != exact"
+
+
+def pin_gemm_f16w_bruteforce(orc, seed=11):
+    """Tiny sizes against the exact rational product A * W16^T, W16 = the FP16
+    weight values (numpy's cast of W * 2^e), scaled back by 2^-e:
+      Full: |S - exact| <= 2^-e sum_k |w16| (2^-22 |a| + 2^-35) * (1 + 2^-40)
+      Base: |S - exact| <= 2^-e sum_k |w16| (2^-11 |a| + 2^-25) * (1 + 2^-40)
+    and Full must beat the Base bound by far, so a dropped or mis-scaled
+    residual product, or a wrong exponent sign, fails."""
+    rng = np.random.default_rng(seed)
+    for (M, N, K) in ((1, 1, 1), (2, 3, 5), (3, 4, 9), (4, 2, 16)):
+        A = (rng.standard_normal((M, K)) * 3.0).astype(np.float32)
+        W = (rng.standard_normal((N, K)) * 0.05).astype(np.float32)
+        e = orc.f16_weight_exponent(float(np.abs(W).max()))
+        w16 = np.ldexp(W.astype(np.float64), e).astype(np.float16).astype(np.float64)
+        Cf, Sf = orc.gemm_f16w(A, W, e, 2)
+        Cb, Sb = orc.gemm_f16w(A, W, e, 1)
+        scale = Fraction(2) ** (-e)
+        for i in range(M):
+            for j in range(N):
+                ex = scale * sum(Fraction(float(A[i, k])) * Fraction(float(w16[j, k]))
+                                 for k in range(K))
+                bf = scale * sum(abs(Fraction(float(w16[j, k]))) *
+                                 (abs(Fraction(float(A[i, k]))) / 2 ** 22 + Fraction(1, 2 ** 35))
+                                 for k in range(K)) * (1 + Fraction(1, 2 ** 40))
+                bb = scale * sum(abs(Fraction(float(w16[j, k]))) *
+                                 (abs(Fraction(float(A[i, k]))) / 2 ** 11 + Fraction(1, 2 ** 25))
+                                 for k in range(K)) * (1 + Fraction(1, 2 ** 40))
+                ef = abs(Fraction(float(Sf[i, j])) - ex)
+                eb = abs(Fraction(float(Sb[i, j])) - ex)
+                assert ef <= bf, "Full (%d,%d,%d) (%d,%d): err %g > bound %g" % (
+                    M, N, K, i, j, float(ef), float(bf))
+                assert eb <= bb, "Base (%d,%d,%d) (%d,%d): err %g > bound %g" % (
+                    M, N, K, i, j, float(eb), float(bb))
+                assert np.float32(float(Sf[i, j])) == Cf[i, j], "Full C is not RNE_fp32(S)"
+
+
+def pin_gemm_f16w_rows(orc, seed=12):
+    rng = np.random.default_rng(seed)
+    A = rng.standard_normal((30, 50)).astype(np.float32)
+    W = rng.standard_normal((20, 50)).astype(np.float32)
+    C, S = orc.gemm_f16w(A, W, 3, 2)
+    rows = np.array([29, 0, 7, 7])
+    Cr, Sr = orc.gemm_f16w(A, W, 3, 2, rows=rows)
+    assert np.array_equal(Sr, S[rows]) and np.array_equal(Cr, C[rows]), "row subset differs"
+
+
+# --------------------------------------------------------------------------
+# INT16 codes and dual-FP16 scores (HEAL+)
+# --------------------------------------------------------------------------
+
+def pin_quantize_i16(orc, seed=13):
+    """INT16 codes: golden values, the range, the extremes, all-zero input, and
+    the paper's INT16 error bound |x - q*D| <= D/2 (D = max|X| / 32767), here
+    with the slack of the two FP32 roundings of the decision."""
+    x = np.array([2.0, -1.0, 0.5, 1e-30, 0.0, -2.0, 1.5], np.float32)
+    q, m = orc.quantize_i16(x)
+    # inv = 32767/2 = 16383.5 exactly; -1 -> -16383.5, a tie, to even -16384;
+    # 0.5 -> 8191.75 -> 8192; 1.5 -> 24575.25 -> 24575
+    assert m == 2.0 and list(q) == [32767, -16384, 8192, 0, 0, -32767, 24575], (list(q), m)
+    # max|X| = 32767 gives inv = 1 exactly, so t = x and halves are ties to even
+    q, m = orc.quantize_i16(np.array([32767.0, 2.5, -3.5, 0.5, 1.5, -0.5, 7.25], np.float32))
+    assert m == 32767.0 and list(q) == [32767, 2, -4, 0, 2, 0, 7], (list(q), m)
+    q0, m0 = orc.quantize_i16(np.zeros(9, np.float32))
+    assert m0 == 0.0 and np.all(q0 == 0), "all-zero tensor"
+    rng = np.random.default_rng(seed)
+    for scale in (1e-3, 1.0, 300.0):
+        x = (rng.standard_normal(50000) * scale).astype(np.float32)
+        x[17] = np.float32(-40.0 * scale)  # an outlier sets max|X|
+        q, m = orc.quantize_i16(x)
+        assert m == np.float32(40.0 * scale)
+        assert q.min() >= -32767 and q.max() <= 32767 and q[17] == -32767
+        D = Fraction(float(m)) / 32767
+        worst = Fraction(0)
+        for i in rng.choice(x.size, 400, replace=False):
+            worst = max(worst, abs(Fraction(float(x[i])) - q[i] * D))
+        assert worst <= D / 2 * (1 + Fraction(1, 2 ** 7)), "INT16 error exceeds D/2"
+
+
+def pin_int16_mse_ratio(orc, seed=14):
+    """The paper's ratio bound E[MSE_fp16] / E[MSE_int16] > 256 sigma^2 / M^2
+    (Section 4, Q/K/V paragraph), measured on Gaussian tensors with one
+    outlier, against numpy's FP16 cast."""
+    rng = np.random.default_rng(seed)
+    for outlier in (4.0, 12.0, 40.0):
+        x = rng.standard_normal(200000).astype(np.float32)
+        x[0] = np.float32(outlier)
+        q, m = orc.quantize_i16(x)
+        deq = q.astype(np.float64) * (float(m) / 32767.0)
+        mse_i16 = np.mean((deq - x) ** 2)
+        mse_f16 = np.mean((x.astype(np.float16).astype(np.float64) - x) ** 2)
+        sigma2, M = np.var(x.astype(np.float64)), float(m)
+        assert mse_f16 / mse_i16 > 256.0 * sigma2 / M ** 2, (outlier, mse_f16 / mse_i16)
+
+
+def pin_unpack_i16_exhaustive(orc):
+    """Every INT16 code q unpacks to FP16 (hi, lo) with hi = numpy's float16 of
+    q, hi + lo / 2^10 == q exactly, and |lo| / 2^10 <= 8."""
+    q = np.arange(-32768, 32768, dtype=np.int64).astype(np.int16)
+    hi, lo = orc.unpack_i16(q)
+    assert np.array_equal(hi, q.astype(np.float16).view(np.uint16)), "hi is not f16(q)"
+    hv, lv = _f16_to_f64(hi), _f16_to_f64(lo)
+    assert np.array_equal(hv + lv / 1024.0, q.astype(np.float64)), "hi + lo/2^10 != q"
+    assert np.abs(lv).max() <= 8 * 1024, "lo out of range"
+
+
+def pin_scores_i16(orc, seed=15):
+    """The four dual-FP16 products sum to the exact integer dot product of the
+    codes (closed form), and C rounds factor * S once, with
+    factor = (maxQ/32767) (maxK/32767) alpha up to three FP32 roundings."""
+    rng = np.random.default_rng(seed)
+    M, N, K = 9, 7, 64
+    Q = rng.integers(-32767, 32768, size=(M, K)).astype(np.int16)
+    Kt = rng.integers(-32767, 32768, size=(N, K)).astype(np.int16)
+    Q[0, :] = 32767
+    Kt[0, :] = -32767
+    mq, mk, alpha = np.float32(2.5), np.float32(0.75), np.float32(1.0 / np.sqrt(128.0))
+    C, S = orc.scores_i16(Q, Kt, mq, mk, alpha)
+    exact = Q.astype(np.int64) @ Kt.astype(np.int64).T
+    assert np.array_equal(S, exact.astype(np.float64)), "scores: S != integer dot product"
+    f = (float(mq) / 32767.0) * (float(mk) / 32767.0) * float(alpha)
+    ref = f * exact.astype(np.float64)
+    assert np.all(np.abs(C - ref) <= np.abs(ref) * 2.0 ** -21), "scores: C != factor * S"
+    rows = np.array([8, 0, 3])
+    Cr, Sr = orc.scores_i16(Q, Kt, mq, mk, alpha, rows=rows)
+    assert np.array_equal(Cr, C[rows]) and np.array_equal(Sr, S[rows]), "row subset differs"
+
+
 SMALL_PINS = [pin_golden_split, pin_split_vs_library, pin_split_properties, pin_golden_gemm,
               pin_bf16_inputs, pin_constructed_split, pin_integer_exact, pin_bruteforce_tiny,
-              pin_alpha, pin_row_subset, pin_nonfinite_propagation]
+              pin_alpha, pin_row_subset, pin_nonfinite_propagation,
+              pin_f16_rne_vs_library, pin_golden_split_f16, pin_split_f16_vs_library,
+              pin_split_f16_properties, pin_weight_exponent, pin_f16_weights_vs_library,
+              pin_gemm_f16w_integer, pin_gemm_f16w_bruteforce, pin_gemm_f16w_rows,
+              pin_quantize_i16, pin_int16_mse_ratio, pin_unpack_i16_exhaustive, pin_scores_i16]

@@ -31,9 +31,41 @@ MUTATIONS = [
     ("nan_not_quiet", "return (uint16_t)(((u >> 16) & 0x8000u) | 0x7fc0u);", "return (uint16_t)(u >> 16);"),
     ("alpha_ignored", "c[j] = (float)((double)alpha * s[j]);", "c[j] = (float)s[j];"),
     ("alpha_after_round", "c[j] = (float)((double)alpha * s[j]);", "c[j] = alpha * (float)s[j];"),
-    ("row_subset_ignored", "int64_t i = rows ? rows[r] : r;", "int64_t i = r < M ? r : M - 1;"),
+    ("row_subset_ignored", "int64_t i = rows ? rows[r] : r;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    split_one(",
+     "int64_t i = r < M ? r : M - 1;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    split_one("),
     ("float_accumulator", "s[j] += a_hi * b_hi + a_hi * b_lo + a_lo * b_hi;",
      "s[j] = (float)(s[j] + (a_hi * b_hi + a_hi * b_lo + a_lo * b_hi));"),
+    # FP16 forms and INT16 scores
+    ("f16_ties_away", "double q = rint(ldexp(a, 10 - E));", "double q = round(ldexp(a, 10 - E));"),
+    ("f16_overflow_at_max", "if (a >= 65520.0) return", "if (a > 65504.0) return"),
+    ("f16_flush_subnormals", "double q = rint(a * 0x1p24);", "double q = 0.0;"),
+    ("f16_lo_not_shifted", "double r = ((double)x - oracle_f16_value(h)) * 1024.0;",
+     "double r = ((double)x - oracle_f16_value(h));"),
+    ("f16_lo_shift_2048", "double r = ((double)x - oracle_f16_value(h)) * 1024.0;",
+     "double r = ((double)x - oracle_f16_value(h)) * 2048.0;"),
+    ("exponent_off_by_one", "while (ldexp(maxabs, e + 1) <= 65504.0) ++e;",
+     "while (ldexp(maxabs, e + 1) < 65504.0) ++e;"),
+    ("exponent_one_too_high", "    return e;\n}", "    return e + 1;\n}"),
+    ("weights_unscaled", "return oracle_f16_rne(ldexp((double)w, e));",
+     "return oracle_f16_rne((double)w);"),
+    ("full_drops_residual", "if (products == 2)", "if (products == 3)"),
+    ("full_residual_2^-11", "ldexp(s_hi + ldexp(s_lo, -10), -e)", "ldexp(s_hi + ldexp(s_lo, -11), -e)"),
+    ("output_scale_sign", "ldexp(s_hi + ldexp(s_lo, -10), -e)", "ldexp(s_hi + ldexp(s_lo, -10), e)"),
+    ("full_residual_subtracted", "ldexp(s_hi + ldexp(s_lo, -10), -e)",
+     "ldexp(s_hi - ldexp(s_lo, -10), -e)"),
+    ("quant_ties_away", "q[i] = (int16_t)rintf(t);", "q[i] = (int16_t)roundf(t);"),
+    ("quant_2^15", "float inv = m > 0.0f ? 32767.0f / m : 0.0f;",
+     "float inv = m > 0.0f ? 32768.0f / m : 0.0f;"),
+    ("quant_truncates", "q[i] = (int16_t)rintf(t);", "q[i] = (int16_t)t;"),
+    ("unpack_lo_unshifted", "*lo = oracle_f16_rne(((double)q - oracle_f16_value(h)) * 1024.0);",
+     "*lo = oracle_f16_rne(((double)q - oracle_f16_value(h)));"),
+    ("scores_drop_lolo", "+ ql[k] * bh[k] + ql[k] * bl[k];", "+ ql[k] * bh[k];"),
+    ("scores_drop_hilo", "s += qh[k] * bh[k] + qh[k] * bl[k] +", "s += qh[k] * bh[k] +"),
+    ("f16w_row_subset_ignored", "int64_t i = rows ? rows[r] : r;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    split_f16_one(",
+     "int64_t i = r < M ? r : M - 1;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    split_f16_one("),
+    ("scores_row_subset_ignored", "int64_t i = rows ? rows[r] : r;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    oracle_unpack_i16(Q",
+     "int64_t i = r < M ? r : M - 1;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    oracle_unpack_i16(Q"),
+    ("scores_no_alpha", "float factor = prod * alpha;", "float factor = prod;"),
 ]
 
 
@@ -53,6 +85,6 @@ def test_mutant_is_caught(tmp_path, source, name, old, new):
     for pin in pins.SMALL_PINS:
         try:
             pin(orc)
-        except AssertionError as e:
+        except Exception as e:  # an assertion, or arithmetic a planted mistake broke
             failures.append((pin.__name__, str(e)[:100]))
     assert failures, "mutation %s passed every pin" % name

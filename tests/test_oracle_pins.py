@@ -17,6 +17,13 @@ def test_split_exhaustive_all_fp32(orc):
         pins.check_split_range_exhaustive(orc, start, chunk)
 
 
+def test_split_f16_exhaustive_all_fp32(orc):
+    """Every FP32 bit pattern gives the HEAL-Full pair the library casts give."""
+    chunk = 1 << 26
+    for start in range(0, 1 << 32, chunk):
+        pins.check_split_f16_range_exhaustive(orc, start, chunk)
+
+
 def test_structured_patterns_cover_rounding_classes():
     bits = pins.structured_patterns()
     low = bits & 0xffff
