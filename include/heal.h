@@ -140,6 +140,140 @@ heal_status_t heal_gemm_f32_instance(int instance, int64_t M, int64_t N, int64_t
 /* The instance heal_gemm_f32 would choose for an M x N output (no HIP call). */
 int heal_gemm_select_instance(int64_t M, int64_t N);
 
+/* ==========================================================================
+ * FP16 forms of the method (HEAL-Base and HEAL-Full), the pre-split B
+ * operand, and the INT16 Q/K score product (HEAL+).
+ *
+ * Packed operands.  A weight or B operand used many times is converted once
+ * into a packed layout in MFMA fragment order: for each block of 16 columns
+ * n (jb = n / 16) and 32-deep chunk of k (kc = k / 32), each plane p holds
+ * 512 16-bit values at
+ *     packed[((jb * KC + kc) * P + p) * 512 + lane * 8 + t],
+ *     lane = (n % 16) + 16 * ((k % 32) / 8),  t = k % 8,  KC = ceil(K / 32),
+ * positions beyond K or N holding +0.  heal_packed_size gives the number of
+ * uint16 values (ceil(N/16) * KC * P * 512); the buffer must be 16-byte
+ * aligned.  K is limited to 2^20 for packed operands.
+ * ========================================================================== */
+
+/*
+ * heal_split_f16 -- the HEAL-Full activation pair on its own (Section 4, GEMM
+ * paragraph: an FP32 activation h becomes h_hi + h_lo / 2^10 in FP16).
+ *   hi[i] = RNE_f16(x[i]),  lo[i] = RNE_f16((x[i] - hi[i]) * 2^10),
+ * as binary16 bit patterns, x - hi and the 2^10 shift exact in FP32.  For
+ * finite |x| < 65520, |x - hi - lo / 2^10| <= 2^-22 |x| + 2^-35.  |x| >= 65520
+ * gives hi = +/-inf and lo = -/+inf; x = +/-inf gives lo = NaN; NaN gives NaN.
+ * Arguments as heal_split_f32.
+ */
+heal_status_t heal_split_f16(const float *x, uint16_t *hi, uint16_t *lo, int64_t n,
+                             hipStream_t stream);
+
+/* Number of uint16 values of a packed K x N operand with `planes` planes (1 or
+ * 2), or -1 for invalid sizes (no HIP call). */
+int64_t heal_packed_size(int64_t K, int64_t N, int planes);
+
+/*
+ * heal_maxabs_f32 -- max|x| over a rows x cols row-major FP32 matrix (row
+ * stride ld >= max(cols, 1)), written as one float to *maxabs (device).  An
+ * empty matrix gives +0.  A NaN element makes the result a NaN pattern.
+ */
+heal_status_t heal_maxabs_f32(const float *x, int64_t rows, int64_t cols, int64_t ld,
+                              float *maxabs, hipStream_t stream);
+
+/*
+ * heal_f16_weight_exponent -- the per-matrix power-of-two weight scale
+ * (Appendix "HEAL Implementation", HEAL-Base: weights are scaled by a power of
+ * two before the FP16 GEMM and the output is scaled back).  *e (host) becomes
+ * the largest integer with maxabs * 2^e <= 65504, so the scaled weights use
+ * the top of the FP16 range and none overflows; maxabs == 0 gives e = 0.
+ * maxabs is a host value (for example read back from heal_maxabs_f32); it must
+ * be finite and >= 0.  No HIP call.
+ */
+heal_status_t heal_f16_weight_exponent(float maxabs, int32_t *e);
+
+/*
+ * heal_pack_f16_weight -- W16 = packed RNE_f16(W * 2^e), one plane, for the
+ * FP16 GEMMs.  W is the FP32 weight of a linear layer, N x K row-major (row
+ * stride ldw >= max(K, 1)), so the GEMM computes A * W^T.  |e| <= 300.  W16
+ * holds heal_packed_size(K, N, 1) values.
+ */
+heal_status_t heal_pack_f16_weight(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t e,
+                                   uint16_t *W16, hipStream_t stream);
+
+/*
+ * heal_gemm_f16w -- FP16 GEMM with FP32 activations and FP32 output:
+ *   products == 1 (HEAL-Base):  C = 2^-e * sum_k f16(a) w16
+ *   products == 2 (HEAL-Full, Section 4 two-product expansion):
+ *       C = 2^-e * (sum_k h_hi w16 + 2^-10 sum_k h_lo w16),
+ *       with (h_hi, h_lo) as heal_split_f16; the two sums are separate FP32
+ *       accumulators, combined by one fused multiply-add and scaled by 2^-e.
+ *   A   : M x K FP32, row stride lda >= max(K, 1);
+ *   W16 : packed FP16 weight from heal_pack_f16_weight (same N, K, e);
+ *   C   : M x N FP32, row stride ldc >= max(N, 1); written, never read.
+ * Reduction order: K in 32-deep chunks ascending, one FP16 MFMA per chunk and
+ * product, so results are bitwise identical run to run and for every M.
+ * FP16 overflow of an activation (|a| >= 65520) gives an infinite head and a
+ * non-finite output, as the FP16 format implies.
+ */
+heal_status_t heal_gemm_f16w(int products, int64_t M, int64_t N, int64_t K, const float *A,
+                             int64_t lda, const uint16_t *W16, int32_t e, float *C, int64_t ldc,
+                             hipStream_t stream);
+heal_status_t heal_gemm_f16w_instance(int instance, int products, int64_t M, int64_t N,
+                                      int64_t K, const float *A, int64_t lda,
+                                      const uint16_t *W16, int32_t e, float *C, int64_t ldc,
+                                      hipStream_t stream);
+
+/*
+ * heal_presplit_b -- the B operand of heal_gemm_f32 split once (as
+ * heal_split_f32) and packed with two planes (hi, lo).  B is K x N with row
+ * stride ldb >= max(N, 1) (trans_b = 0), or N x K with ldb >= max(K, 1)
+ * (trans_b = 1, a linear layer's weight).  Bp holds heal_packed_size(K, N, 2)
+ * values: the same 4 bytes per element as the FP32 operand.
+ *
+ * heal_gemm_f32_presplit -- C = A * B from the pre-split operand: the same
+ * bf16 MFMAs in the same order as heal_gemm_f32, so C is bitwise equal to
+ * heal_gemm_f32(A, B) (and to the strided-batched form with trans_b = 1 on the
+ * transposed storage); no B element is split on this path.
+ */
+heal_status_t heal_presplit_b(const float *B, int64_t K, int64_t N, int64_t ldb, int trans_b,
+                              uint16_t *Bp, hipStream_t stream);
+heal_status_t heal_gemm_f32_presplit(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda,
+                                     const uint16_t *Bp, float *C, int64_t ldc,
+                                     hipStream_t stream);
+heal_status_t heal_gemm_f32_presplit_instance(int instance, int64_t M, int64_t N, int64_t K,
+                                              const float *A, int64_t lda, const uint16_t *Bp,
+                                              float *C, int64_t ldc, hipStream_t stream);
+
+/*
+ * heal_quantize_i16 -- INT16 storage of a tensor (Section 4, Q/K/V
+ * paragraph): q[i] = Round(32767 x[i] / max|x|), the decision taken in FP32 as
+ * inv = 32767 / m, t = x * inv, q = t rounded to nearest, ties to even; every
+ * code lies in [-32767, 32767].  m = max|x| is written to *maxabs (device) and
+ * is the tensor's dequantisation scale (x ~ q * m / 32767).  An all-zero
+ * tensor gives m = 0 and zero codes.  x must be finite.  Two kernels are
+ * enqueued (the maximum, then the codes); no host synchronisation.
+ */
+heal_status_t heal_quantize_i16(const float *x, int64_t n, int16_t *q, float *maxabs,
+                                hipStream_t stream);
+
+/*
+ * heal_scores_i16 -- attention scores from INT16 Q and K with the dual-FP16
+ * expansion (Section 4, displayed attention expansion):
+ *   S_b = f * (Q_hi + Q_lo/2^10)(K_hi + K_lo/2^10)^T,
+ *   f = ((maxQ / 32767) * (maxK / 32767)) * alpha, each step in FP32,
+ * where each code q unpacks exactly into hi = RNE_f16(q) and
+ * lo/2^10 = q - hi; all four products are accumulated in FP32 (per 32-deep
+ * chunk: hi*hi, hi*lo, lo*hi, lo*lo), so the sum is the integer dot product
+ * of the codes up to FP32 accumulation.
+ *   Q_b  = Q + b*strideQ : M x K INT16, row stride ldq >= max(K, 1);
+ *   K_b  = Kt + b*strideK: N x K INT16 (keys, one row per position), ldk >= max(K, 1);
+ *   maxQ, maxK : device floats, the maxima written by heal_quantize_i16;
+ *   S_b  = S + b*strideS : M x N FP32, row stride lds >= max(N, 1).
+ */
+heal_status_t heal_scores_i16(int64_t M, int64_t N, int64_t K, const int16_t *Q, int64_t ldq,
+                              int64_t strideQ, const float *maxQ, const int16_t *Kt, int64_t ldk,
+                              int64_t strideK, const float *maxK, float alpha, float *S,
+                              int64_t lds, int64_t strideS, int64_t batch, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,5 +1,6 @@
 // C ABI of libheal.so: argument validation, device check, instance choice.
 // Every argument check runs before the first HIP call.
+#include <math.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -100,6 +101,44 @@ heal_status_t run_gemm(int instance, int64_t M, int64_t N, int64_t K, float alph
     return e == hipSuccess ? HEAL_OK : HEAL_ERR_LAUNCH;
 }
 
+// Packed operands: K bounded so that every byte offset inside one tile of
+// packed B stays below 2^31 (16 blocks x ceil(K/32) chunks x 2 planes x 1 KiB).
+constexpr int64_t kMaxPackedK = (int64_t)1 << 20;
+constexpr int32_t kMaxExponent = 300;
+
+// Products of an FP32 A with a packed B (HEAL-Base / HEAL-Full weights, the
+// pre-split bf16 operand).
+heal_status_t run_packed(int op, int instance, int64_t M, int64_t N, int64_t K, const float *A,
+                         int64_t lda, const uint16_t *Bp, int32_t e, float *C, int64_t ldc,
+                         hipStream_t stream)
+{
+    if (M < 0 || N < 0 || K < 0 || K > kMaxPackedK) return HEAL_ERR_INVALID_VALUE;
+    const int64_t lim = (int64_t)1 << 48;
+    if (M > lim || N > ((int64_t)1 << 40) || lda > lim || ldc > lim) return HEAL_ERR_INVALID_VALUE;
+    if (lda < (K > 1 ? K : 1) || ldc < (N > 1 ? N : 1)) return HEAL_ERR_INVALID_VALUE;
+    if (instance < 0 || instance >= HEAL_INSTANCE_COUNT) return HEAL_ERR_INVALID_VALUE;
+    if (M == 0 || N == 0) return HEAL_OK;
+    if (!C || !aligned4(C)) return HEAL_ERR_INVALID_VALUE;
+    if (K > 0 && (!A || !Bp || !aligned4(A) || !aligned16(Bp))) return HEAL_ERR_INVALID_VALUE;
+    heal_status_t st = check_device();
+    if (st != HEAL_OK) return st;
+    heal::OpArgs a = {};
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    a.A = A;
+    a.lda = lda;
+    a.B = Bp;
+    a.C = C;
+    a.ldc = ldc;
+    a.batch = 1;
+    a.e = e;
+    a.alpha = 1.0f;
+    a.vecA = aligned16(A) && lda % 4 == 0;
+    a.vecC = aligned16(C) && ldc % 4 == 0;
+    return heal::launch_gemm_op(op, instance, a, stream) == hipSuccess ? HEAL_OK : HEAL_ERR_LAUNCH;
+}
+
 }  // namespace
 
 extern "C" {
@@ -158,5 +197,176 @@ heal_status_t heal_gemm_f32_instance(int instance, int64_t M, int64_t N, int64_t
 }
 
 int heal_gemm_select_instance(int64_t M, int64_t N) { return select_instance(M, N); }
+
+// ---- FP16 forms, pre-split operand, INT16 scores ----------------------------
+
+heal_status_t heal_split_f16(const float *x, uint16_t *hi, uint16_t *lo, int64_t n,
+                             hipStream_t stream)
+{
+    if (n < 0) return HEAL_ERR_INVALID_VALUE;
+    if (n == 0) return HEAL_OK;
+    if (!x || !hi || !lo || !aligned4(x) || (reinterpret_cast<uintptr_t>(hi) & 1u) ||
+        (reinterpret_cast<uintptr_t>(lo) & 1u))
+        return HEAL_ERR_INVALID_VALUE;
+    heal_status_t st = check_device();
+    if (st != HEAL_OK) return st;
+    return heal::launch_split_f16(x, hi, lo, n, stream) == hipSuccess ? HEAL_OK : HEAL_ERR_LAUNCH;
+}
+
+int64_t heal_packed_size(int64_t K, int64_t N, int planes)
+{
+    if (K < 0 || N < 0 || (planes != 1 && planes != 2) || K > kMaxPackedK || N > ((int64_t)1 << 40))
+        return -1;
+    return ((N + 15) / 16) * ((K + 31) / 32) * planes * 512;
+}
+
+heal_status_t heal_maxabs_f32(const float *x, int64_t rows, int64_t cols, int64_t ld,
+                              float *maxabs, hipStream_t stream)
+{
+    if (rows < 0 || cols < 0 || ld < (cols > 1 ? cols : 1) || !maxabs || !aligned4(maxabs))
+        return HEAL_ERR_INVALID_VALUE;
+    if (rows > ((int64_t)1 << 40) || ld > ((int64_t)1 << 40)) return HEAL_ERR_INVALID_VALUE;
+    if (rows > 0 && cols > 0 && (!x || !aligned4(x))) return HEAL_ERR_INVALID_VALUE;
+    heal_status_t st = check_device();
+    if (st != HEAL_OK) return st;
+    return heal::launch_maxabs(x, rows, cols, ld, maxabs, stream) == hipSuccess ? HEAL_OK
+                                                                                 : HEAL_ERR_LAUNCH;
+}
+
+heal_status_t heal_f16_weight_exponent(float maxabs, int32_t *e)
+{
+    if (!e || !(maxabs >= 0.0f) || maxabs > 3.4028235e38f) return HEAL_ERR_INVALID_VALUE;
+    int32_t r = 0;
+    if (maxabs > 0.0f) {
+        // largest r with maxabs * 2^r <= 65504 (exact in double)
+        const double m = (double)maxabs;
+        while (ldexp(m, r) > 65504.0) --r;
+        while (ldexp(m, r + 1) <= 65504.0) ++r;
+    }
+    *e = r;
+    return HEAL_OK;
+}
+
+heal_status_t heal_pack_f16_weight(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t e,
+                                   uint16_t *W16, hipStream_t stream)
+{
+    if (N < 0 || K < 0 || K > kMaxPackedK || N > ((int64_t)1 << 40) ||
+        ldw < (K > 1 ? K : 1) || e < -kMaxExponent || e > kMaxExponent)
+        return HEAL_ERR_INVALID_VALUE;
+    if (N == 0 || K == 0) return HEAL_OK;
+    if (!W || !W16 || !aligned4(W) || !aligned16(W16)) return HEAL_ERR_INVALID_VALUE;
+    heal_status_t st = check_device();
+    if (st != HEAL_OK) return st;
+    return heal::launch_pack(0, W, K, N, ldw, true, e, W16, stream) == hipSuccess
+               ? HEAL_OK
+               : HEAL_ERR_LAUNCH;
+}
+
+heal_status_t heal_presplit_b(const float *B, int64_t K, int64_t N, int64_t ldb, int trans_b,
+                              uint16_t *Bp, hipStream_t stream)
+{
+    if (N < 0 || K < 0 || K > kMaxPackedK || N > ((int64_t)1 << 40) ||
+        (trans_b != 0 && trans_b != 1))
+        return HEAL_ERR_INVALID_VALUE;
+    if (ldb < (trans_b ? (K > 1 ? K : 1) : (N > 1 ? N : 1))) return HEAL_ERR_INVALID_VALUE;
+    if (N == 0 || K == 0) return HEAL_OK;
+    if (!B || !Bp || !aligned4(B) || !aligned16(Bp)) return HEAL_ERR_INVALID_VALUE;
+    heal_status_t st = check_device();
+    if (st != HEAL_OK) return st;
+    return heal::launch_pack(1, B, K, N, ldb, trans_b != 0, 0, Bp, stream) == hipSuccess
+               ? HEAL_OK
+               : HEAL_ERR_LAUNCH;
+}
+
+heal_status_t heal_gemm_f16w_instance(int instance, int products, int64_t M, int64_t N,
+                                      int64_t K, const float *A, int64_t lda,
+                                      const uint16_t *W16, int32_t e, float *C, int64_t ldc,
+                                      hipStream_t stream)
+{
+    if (products != 1 && products != 2) return HEAL_ERR_INVALID_VALUE;
+    if (e < -kMaxExponent || e > kMaxExponent) return HEAL_ERR_INVALID_VALUE;
+    return run_packed(products == 1 ? heal::OP_BASE : heal::OP_FULL, instance, M, N, K, A, lda,
+                      W16, e, C, ldc, stream);
+}
+
+heal_status_t heal_gemm_f16w(int products, int64_t M, int64_t N, int64_t K, const float *A,
+                             int64_t lda, const uint16_t *W16, int32_t e, float *C, int64_t ldc,
+                             hipStream_t stream)
+{
+    return heal_gemm_f16w_instance(HEAL_INSTANCE_AUTO, products, M, N, K, A, lda, W16, e, C, ldc,
+                                   stream);
+}
+
+heal_status_t heal_gemm_f32_presplit_instance(int instance, int64_t M, int64_t N, int64_t K,
+                                              const float *A, int64_t lda, const uint16_t *Bp,
+                                              float *C, int64_t ldc, hipStream_t stream)
+{
+    return run_packed(heal::OP_PRESPLIT, instance, M, N, K, A, lda, Bp, 0, C, ldc, stream);
+}
+
+heal_status_t heal_gemm_f32_presplit(int64_t M, int64_t N, int64_t K, const float *A, int64_t lda,
+                                     const uint16_t *Bp, float *C, int64_t ldc, hipStream_t stream)
+{
+    return run_packed(heal::OP_PRESPLIT, HEAL_INSTANCE_AUTO, M, N, K, A, lda, Bp, 0, C, ldc,
+                      stream);
+}
+
+heal_status_t heal_quantize_i16(const float *x, int64_t n, int16_t *q, float *maxabs,
+                                hipStream_t stream)
+{
+    if (n < 0 || n > ((int64_t)1 << 40) || !maxabs || !aligned4(maxabs))
+        return HEAL_ERR_INVALID_VALUE;
+    if (n > 0 && (!x || !q || !aligned4(x) || (reinterpret_cast<uintptr_t>(q) & 1u)))
+        return HEAL_ERR_INVALID_VALUE;
+    heal_status_t st = check_device();
+    if (st != HEAL_OK) return st;
+    return heal::launch_quantize(x, n, q, maxabs, stream) == hipSuccess ? HEAL_OK
+                                                                        : HEAL_ERR_LAUNCH;
+}
+
+heal_status_t heal_scores_i16(int64_t M, int64_t N, int64_t K, const int16_t *Q, int64_t ldq,
+                              int64_t strideQ, const float *maxQ, const int16_t *Kt, int64_t ldk,
+                              int64_t strideK, const float *maxK, float alpha, float *S,
+                              int64_t lds, int64_t strideS, int64_t batch, hipStream_t stream)
+{
+    if (M < 0 || N < 0 || K < 0 || batch < 0) return HEAL_ERR_INVALID_VALUE;
+    if (strideQ < 0 || strideK < 0 || strideS < 0) return HEAL_ERR_INVALID_VALUE;
+    if (ldq < (K > 1 ? K : 1) || ldk < (K > 1 ? K : 1) || lds < (N > 1 ? N : 1))
+        return HEAL_ERR_INVALID_VALUE;
+    const int64_t lim = (int64_t)1 << 48;
+    if (M > lim || N > lim || K > lim || ldq > lim || ldk > lim || lds > lim || batch > lim)
+        return HEAL_ERR_INVALID_VALUE;
+    if (M == 0 || N == 0 || batch == 0) return HEAL_OK;
+    if (!S || !aligned4(S) || !maxQ || !maxK || !aligned4(maxQ) || !aligned4(maxK))
+        return HEAL_ERR_INVALID_VALUE;
+    if (K > 0 && (!Q || !Kt || (reinterpret_cast<uintptr_t>(Q) & 1u) ||
+                  (reinterpret_cast<uintptr_t>(Kt) & 1u)))
+        return HEAL_ERR_INVALID_VALUE;
+    heal_status_t st = check_device();
+    if (st != HEAL_OK) return st;
+    heal::OpArgs a = {};
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    a.A = Q;
+    a.lda = ldq;
+    a.strideA = strideQ;
+    a.B = Kt;
+    a.ldb = ldk;
+    a.strideB = strideK;
+    a.C = S;
+    a.ldc = lds;
+    a.strideC = strideS;
+    a.batch = batch;
+    a.maxA = maxQ;
+    a.maxB = maxK;
+    a.alpha = alpha;
+    a.vecA = aligned16(Q) && ldq % 8 == 0 && (batch == 1 || strideQ % 8 == 0);
+    a.vecB = aligned16(Kt) && ldk % 8 == 0 && (batch == 1 || strideK % 8 == 0);
+    a.vecC = aligned16(S) && lds % 4 == 0 && (batch == 1 || strideS % 4 == 0);
+    return heal::launch_gemm_op(heal::OP_SCORES, HEAL_INSTANCE_AUTO, a, stream) == hipSuccess
+               ? HEAL_OK
+               : HEAL_ERR_LAUNCH;
+}
 
 }  // extern "C"

@@ -19,6 +19,8 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 // Split two FP32 values into packed bf16 pairs (element 0 in the low half):
 //   hi = RNE_bf16(x)          -- one v_cvt_pk_bf16_f32 for both elements
@@ -35,6 +37,46 @@ __device__ __forceinline__ void split2(float x0, float x1, uint32_t &hi, uint32_
     f32x2 r = {x0 - __builtin_bit_cast(float, hi << 16),
                x1 - __builtin_bit_cast(float, hi & 0xffff0000u)};
     lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, bf16x2));
+}
+
+// HEAL-Full pair of two FP32 values, packed binary16 (element 0 in the low half):
+//   hi = RNE_f16(x)                 -- one v_cvt_pk_f16_f32 for both elements
+//   lo = RNE_f16((x - hi) * 2^10)   -- widen hi, subtract, shift, convert
+// (HEAL Section 4, GEMM paragraph: the activation becomes an FP16 head plus an
+// FP16 residual shifted up by 2^10 so that it keeps FP16's normal range).
+// x - hi is exact in FP32 and so is the 2^10 shift (|x - hi| <= 2^4 below the
+// overflow threshold); an infinite head gives lo = -/+inf or NaN by IEEE rules.
+__device__ __forceinline__ void split2_f16(float x0, float x1, uint32_t &hi, uint32_t &lo)
+{
+    f32x2 v = {x0, x1};
+    f16x2 h = __builtin_convertvector(v, f16x2);
+    f32x2 hf = __builtin_convertvector(h, f32x2);
+    f32x2 r = {(x0 - hf.x) * 1024.0f, (x1 - hf.y) * 1024.0f};
+    hi = __builtin_bit_cast(uint32_t, h);
+    lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, f16x2));
+}
+
+// RNE_f16 of two FP32 values, packed (the single cast of HEAL-Base).
+__device__ __forceinline__ uint32_t cvt2_f16(float x0, float x1)
+{
+    f32x2 v = {x0, x1};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2));
+}
+
+// Dual-FP16 pair of two INT16 codes q (HEAL Section 4, Q/K/V paragraph):
+// hi = RNE_f16(q) and the remainder q - hi, an integer with |q - hi| <= 8,
+// both exact in FP16, so hi + (q - hi) == q.  The remainder is the paper's
+// lower half divided by 2^10; feeding it to the matrix unit instead of the
+// shifted half and scaling its products back by 2^-10 gives the same exact
+// products.
+__device__ __forceinline__ void unpack2_i16(int q0, int q1, uint32_t &hi, uint32_t &lo)
+{
+    f32x2 v = {(float)q0, (float)q1};
+    f16x2 h = __builtin_convertvector(v, f16x2);
+    f32x2 hf = __builtin_convertvector(h, f32x2);
+    f32x2 r = {v.x - hf.x, v.y - hf.y};
+    hi = __builtin_bit_cast(uint32_t, h);
+    lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, f16x2));
 }
 
 }  // namespace heal

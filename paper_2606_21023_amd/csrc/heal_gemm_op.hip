@@ -1,0 +1,528 @@
+// GEMM kernels of the FP16 and INT16 forms of the method, and of the bf16x3
+// product with a pre-split B operand, for gfx950 (MI355X).
+//
+//   OP_BASE     HEAL-Base (Appendix "HEAL Implementation"): the FP32 activation
+//               is cast once to FP16 and multiplied by the FP16 weight, which
+//               was scaled by a per-matrix power of two 2^e;
+//               C = 2^-e * sum_k f16(a) w16.
+//   OP_FULL     HEAL-Full (Section 4, GEMM paragraph and its two-product
+//               expansion): the activation is the pair h_hi = f16(h),
+//               h_lo = f16((h - h_hi) 2^10); two products into two FP32
+//               accumulators, combined once at the end:
+//               C = 2^-e * (acc_hi + 2^-10 acc_lo).
+//   OP_SCORES   HEAL+ score product (Section 4, Q/K/V paragraph and its
+//               attention expansion): INT16 codes of Q and K are unpacked into
+//               dual-FP16 pairs and all four products are accumulated:
+//               C = ((maxQ/32767)(maxK/32767) alpha) * sum_k qQ qK.
+//   OP_PRESPLIT the bf16x3 compensated product of heal_gemm_f32 with B already
+//               split into bf16 (hi, lo) and packed: the same MFMAs in the same
+//               order, so the result is bitwise equal to heal_gemm_f32.
+//
+// Data path of one workgroup (one BM x BN output tile):
+//   A (row-major FP32 or INT16) --16-byte loads--> VGPRs --convert / split-->
+//   LDS planes (k-contiguous rows, XOR-swizzled);
+//   B packed in MFMA fragment order (16 columns x 32 k per 1 KiB block and
+//   plane) --16-byte loads--> VGPRs --copy--> LDS (no swizzle: each lane
+//   reads its own 16 bytes of a block, consecutive lanes consecutive
+//   addresses), or B as INT16 rows converted like A;
+//   two LDS stages, one barrier per stage; v_mfma_f32_16x16x32_{f16,bf16}.
+//
+// Reduction order, identical in every instance of one product (so results
+// are bitwise equal run to run and for every M): K is walked in 32-deep
+// chunks in ascending order; per chunk the products are added in a fixed
+// order (listed at each product); the K tail and out-of-range rows and
+// columns are zero-filled.  No split-K and no atomics.
+//
+// MFMA operand roles as in the bf16x3 kernels: the B fragment is the first
+// source (16 output columns n), the A fragment the second (16 output rows m),
+// so each lane's accumulator is C[m][n..n+3].
+#include "heal.h"
+#include "heal_device.h"
+#include "heal_internal.h"
+
+namespace heal {
+
+namespace {
+
+template <int OP>
+struct OpT;
+// AP, BP: LDS planes of A and B; NACC: accumulators per output block;
+// A_I16: A holds INT16 codes; B_ROWS: B is INT16 N x K rows (else packed).
+template <>
+struct OpT<OP_BASE> {
+    static constexpr int AP = 1, BP = 1, NACC = 1;
+    static constexpr bool A_I16 = false, B_ROWS = false;
+};
+template <>
+struct OpT<OP_FULL> {
+    static constexpr int AP = 2, BP = 1, NACC = 2;
+    static constexpr bool A_I16 = false, B_ROWS = false;
+};
+template <>
+struct OpT<OP_SCORES> {
+    static constexpr int AP = 2, BP = 2, NACC = 1;
+    static constexpr bool A_I16 = true, B_ROWS = true;
+};
+template <>
+struct OpT<OP_PRESPLIT> {
+    static constexpr int AP = 2, BP = 2, NACC = 1;
+    static constexpr bool A_I16 = false, B_ROWS = false;
+};
+
+template <bool BF16>
+__device__ __forceinline__ f32x4 mma(u32x4 b, u32x4 a, f32x4 c)
+{
+    if constexpr (BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, b),
+                                                       __builtin_bit_cast(bf16x8, a), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, b),
+                                                      __builtin_bit_cast(f16x8, a), c, 0, 0, 0);
+}
+
+constexpr int kRsrcFlags = 0x00020000;  // raw buffer, 32-bit data format
+constexpr uint32_t kOOB = 0x80000000u;  // offset beyond num_records: the load returns zeros
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, 0x7fffffff,
+                                             kRsrcFlags);
+}
+
+__device__ __forceinline__ u32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff)
+{
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, 0));
+}
+
+template <int OP, int BM, int BN, int WM, int WN, int NT, int BK, bool VEC>
+__global__ void __launch_bounds__(NT)
+gemm_op_kernel(OpArgs p)
+{
+    using O = OpT<OP>;
+    constexpr int ROWB = BK * 2;                 // bytes per LDS row of one plane
+    constexpr int NCH = BK / 8;                  // 16-byte chunks per row
+    constexpr int RPW = BK >= 64 ? 1 : 64 / BK;  // rows sharing one 128-byte window
+    constexpr int SWM = (NCH < 8 ? NCH : 8) - 1; // XOR swizzle mask on the chunk index
+    constexpr int KS = BK / 32;                  // MFMA chunks per stage
+    constexpr int A_PLANE = BM * ROWB;
+    constexpr int B_PLANE = BN * ROWB;
+    constexpr int STAGE = O::AP * A_PLANE + O::BP * B_PLANE;
+    constexpr int WAVES_M = BM / WM;
+    constexpr int FM = WM / 16, FN = WN / 16;
+    static_assert(BK % 32 == 0 && BK <= 128, "stage depth");
+    static_assert(BM % WM == 0 && BN % WN == 0 && WM % 16 == 0 && WN % 16 == 0, "wave tiling");
+    static_assert(WAVES_M * (BN / WN) * 64 == NT, "every wave computes one wave tile");
+
+    // 16-byte load units of one stage
+    constexpr int A_EPU = O::A_I16 ? 8 : 4;      // A elements per unit
+    constexpr int A_UPR = BK / A_EPU;            // units per A row
+    constexpr int A_UNITS = BM * A_UPR;
+    constexpr int A_IT = (A_UNITS + NT - 1) / NT;
+    constexpr int B_UPR = BK / 8;                // INT16 B rows: units per row
+    constexpr int B_BLK = KS * O::BP * 64;       // packed B: units per 16-column block
+    constexpr int B_UNITS = O::B_ROWS ? BN * B_UPR : (BN / 16) * B_BLK;
+    constexpr int B_IT = (B_UNITS + NT - 1) / NT;
+    constexpr int ESZ_A = O::A_I16 ? 2 : 4;
+
+    __shared__ __attribute__((aligned(16))) char smem0[STAGE];
+    __shared__ __attribute__((aligned(16))) char smem1[STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int fr = lane & 15;
+    const int fg = lane >> 4;
+    const int wm = wave % WAVES_M;
+    const int wn = wave / WAVES_M;
+
+    auto swz = [](int row) { return (row / RPW) & SWM; };
+    auto chunk_off = [&](int row, int c) { return row * ROWB + ((c ^ swz(row)) << 4); };
+    auto quad_off = [&](int row, int kq) {
+        return row * ROWB + (((kq >> 1) ^ swz(row)) << 4) + ((kq & 1) << 3);
+    };
+
+    // ---- tile coordinates: XCD-aware, grouped along M (as the bf16x3 kernels)
+    const int64_t tiles_m = (p.M + BM - 1) / BM;
+    const int64_t tiles_n = (p.N + BN - 1) / BN;
+    const int64_t nb = (int64_t)gridDim.x;
+    int64_t bid = blockIdx.x;
+    {
+        const int64_t x = bid & 7, i = bid >> 3, q = nb >> 3, r = nb & 7;
+        bid = x * q + (x < r ? x : r) + i;
+    }
+    constexpr int GM = HEAL_GROUP_M;
+    const int64_t group = bid / (GM * tiles_n);
+    const int64_t first_m = group * GM;
+    const int64_t gm = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
+    const int64_t in_group = bid - group * GM * tiles_n;
+    const int64_t m0 = (first_m + in_group % gm) * BM;
+    const int64_t n0 = (in_group / gm) * BN;
+
+    const int64_t M = p.M, N = p.N, K = p.K;
+    const int64_t nk = (K + BK - 1) / BK;
+    const int64_t KC = (K + 31) / 32;            // packed B: chunks per column block
+    const int64_t NB16 = (N + 15) / 16;          // packed B: column blocks
+
+    for (int64_t b = blockIdx.y; b < p.batch; b += gridDim.y) {
+        const char *Ab = reinterpret_cast<const char *>(p.A) + b * p.strideA * ESZ_A;
+        const char *Bb = reinterpret_cast<const char *>(p.B) + b * p.strideB * 2;
+        float *__restrict__ C = p.C + b * p.strideC;
+
+        const __amdgpu_buffer_rsrc_t rsrc_a = make_rsrc(Ab + m0 * p.lda * ESZ_A);
+        const __amdgpu_buffer_rsrc_t rsrc_b =
+            O::B_ROWS ? make_rsrc(Bb + n0 * p.ldb * 2)
+                      : make_rsrc(Bb + (n0 / 16) * KC * O::BP * 1024);
+
+        f32x4 acc[O::NACC][FN][FM];
+#pragma unroll
+        for (int a = 0; a < O::NACC; ++a)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int i = 0; i < FM; ++i) acc[a][j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+        u32x4 ra[A_IT], rb[B_IT];
+
+        // ---- global -> registers for the stage starting at k0 -------------
+        auto load_stage = [&](int64_t k0) {
+#pragma unroll
+            for (int it = 0; it < A_IT; ++it) {
+                const int u = it * NT + tid;
+                if (A_UNITS % NT != 0 && u >= A_UNITS) continue;
+                const int row = u / A_UPR, c = u % A_UPR;
+                const int64_t k = k0 + (int64_t)c * A_EPU;
+                const bool ok = m0 + row < M && k < K;
+                if (VEC) {
+                    const uint32_t off =
+                        ok ? (uint32_t)(((int64_t)row * p.lda + k) * ESZ_A) : kOOB;
+                    ra[it] = bload(rsrc_a, off);
+                } else {
+                    u32x4 v = {0u, 0u, 0u, 0u};
+                    if (m0 + row < M) {
+                        const char *rp = Ab + ((m0 + row) * p.lda + k) * ESZ_A;
+                        if (O::A_I16) {
+                            const int16_t *q = reinterpret_cast<const int16_t *>(rp);
+#pragma unroll
+                            for (int t = 0; t < 8; t += 2) {
+                                const uint32_t lo16 = k + t < K ? (uint16_t)q[t] : 0u;
+                                const uint32_t hi16 = k + t + 1 < K ? (uint16_t)q[t + 1] : 0u;
+                                v[t / 2] = lo16 | (hi16 << 16);
+                            }
+                        } else {
+                            const float *f = reinterpret_cast<const float *>(rp);
+#pragma unroll
+                            for (int t = 0; t < 4; ++t)
+                                v[t] = k + t < K ? __builtin_bit_cast(uint32_t, f[t]) : 0u;
+                        }
+                    }
+                    ra[it] = v;
+                }
+            }
+#pragma unroll
+            for (int it = 0; it < B_IT; ++it) {
+                const int u = it * NT + tid;
+                if (B_UNITS % NT != 0 && u >= B_UNITS) continue;
+                if (O::B_ROWS) {
+                    const int row = u / B_UPR, c = u % B_UPR;
+                    const int64_t k = k0 + 8 * (int64_t)c;
+                    if (VEC) {
+                        const bool ok = n0 + row < N && k < K;
+                        const uint32_t off =
+                            ok ? (uint32_t)(((int64_t)row * p.ldb + k) * 2) : kOOB;
+                        rb[it] = bload(rsrc_b, off);
+                    } else {
+                        u32x4 v = {0u, 0u, 0u, 0u};
+                        if (n0 + row < N) {
+                            const int16_t *q = reinterpret_cast<const int16_t *>(Bb) +
+                                               (n0 + row) * p.ldb + k;
+#pragma unroll
+                            for (int t = 0; t < 8; t += 2) {
+                                const uint32_t lo16 = k + t < K ? (uint16_t)q[t] : 0u;
+                                const uint32_t hi16 = k + t + 1 < K ? (uint16_t)q[t + 1] : 0u;
+                                v[t / 2] = lo16 | (hi16 << 16);
+                            }
+                        }
+                        rb[it] = v;
+                    }
+                } else {
+                    // packed: block j of the tile, unit r = (ks * BP + plane) * 64 + lane
+                    const int j = u / B_BLK, r = u % B_BLK;
+                    const int64_t kc = k0 / 32 + r / (O::BP * 64);
+                    const bool ok = n0 / 16 + j < NB16 && kc < KC;
+                    const uint32_t off =
+                        ok ? (uint32_t)(((int64_t)j * KC * O::BP * 64 + (k0 / 32) * O::BP * 64 + r) *
+                                        16)
+                           : kOOB;
+                    rb[it] = bload(rsrc_b, off);
+                }
+            }
+        };
+
+        // ---- registers -> LDS: convert A (and INT16 B), copy packed B -----
+        auto store_stage = [&](char *s) {
+            char *a0 = s, *a1 = s + A_PLANE;
+            char *b0 = s + O::AP * A_PLANE, *b1 = b0 + B_PLANE;
+#pragma unroll
+            for (int it = 0; it < A_IT; ++it) {
+                const int u = it * NT + tid;
+                if (A_UNITS % NT != 0 && u >= A_UNITS) continue;
+                const int row = u / A_UPR, c = u % A_UPR;
+                const u32x4 v = ra[it];
+                if constexpr (O::A_I16) {
+                    u32x4 h, l;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        uint32_t hh, ll;
+                        unpack2_i16((int)(int16_t)(v[t] & 0xffffu), (int)(int16_t)(v[t] >> 16), hh,
+                                    ll);
+                        h[t] = hh;
+                        l[t] = ll;
+                    }
+                    const int off = chunk_off(row, c);
+                    *reinterpret_cast<u32x4 *>(a0 + off) = h;
+                    *reinterpret_cast<u32x4 *>(a1 + off) = l;
+                } else {
+                    // bit-cast the whole vector: this compiler turns a bit-cast of
+                    // one vector element into a read of element 0
+                    const f32x4 xf = __builtin_bit_cast(f32x4, v);
+                    const float x0 = xf.x, x1 = xf.y, x2 = xf.z, x3 = xf.w;
+                    const int off = quad_off(row, c);
+                    if constexpr (OP == OP_BASE) {
+                        const u32x2 h = {cvt2_f16(x0, x1), cvt2_f16(x2, x3)};
+                        *reinterpret_cast<u32x2 *>(a0 + off) = h;
+                    } else {
+                        uint32_t h0, l0, h1, l1;
+                        if constexpr (OP == OP_FULL) {
+                            split2_f16(x0, x1, h0, l0);
+                            split2_f16(x2, x3, h1, l1);
+                        } else {
+                            split2(x0, x1, h0, l0);
+                            split2(x2, x3, h1, l1);
+                        }
+                        const u32x2 h = {h0, h1}, l = {l0, l1};
+                        *reinterpret_cast<u32x2 *>(a0 + off) = h;
+                        *reinterpret_cast<u32x2 *>(a1 + off) = l;
+                    }
+                }
+            }
+#pragma unroll
+            for (int it = 0; it < B_IT; ++it) {
+                const int u = it * NT + tid;
+                if (B_UNITS % NT != 0 && u >= B_UNITS) continue;
+                const u32x4 v = rb[it];
+                if constexpr (O::B_ROWS) {
+                    const int row = u / B_UPR, c = u % B_UPR;
+                    u32x4 h, l;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        uint32_t hh, ll;
+                        unpack2_i16((int)(int16_t)(v[t] & 0xffffu), (int)(int16_t)(v[t] >> 16), hh,
+                                    ll);
+                        h[t] = hh;
+                        l[t] = ll;
+                    }
+                    const int off = chunk_off(row, c);
+                    *reinterpret_cast<u32x4 *>(b0 + off) = h;
+                    *reinterpret_cast<u32x4 *>(b1 + off) = l;
+                } else {
+                    *reinterpret_cast<u32x4 *>(b0 + u * 16) = v;
+                }
+            }
+        };
+
+        // ---- LDS -> fragments -> MFMA, one stage -------------------------
+        auto compute_stage = [&](const char *s) {
+            const char *a0 = s, *a1 = s + A_PLANE;
+            const char *b0 = s + O::AP * A_PLANE, *b1 = b0 + B_PLANE;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                u32x4 ah[FM], al[FM];
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    const int off = chunk_off(wm * WM + i * 16 + fr, ks * 4 + fg);
+                    ah[i] = *reinterpret_cast<const u32x4 *>(a0 + off);
+                    if (O::AP == 2) al[i] = *reinterpret_cast<const u32x4 *>(a1 + off);
+                }
+#pragma unroll
+                for (int j = 0; j < FN; ++j) {
+                    u32x4 bh, bl;
+                    if constexpr (O::B_ROWS) {
+                        const int off = chunk_off(wn * WN + j * 16 + fr, ks * 4 + fg);
+                        bh = *reinterpret_cast<const u32x4 *>(b0 + off);
+                        bl = *reinterpret_cast<const u32x4 *>(b1 + off);
+                    } else {
+                        const int blk = (wn * FN + j) * KS + ks;
+                        const int off = blk * O::BP * 1024 + lane * 16;
+                        bh = *reinterpret_cast<const u32x4 *>(b0 + off);
+                        if (O::BP == 2) bl = *reinterpret_cast<const u32x4 *>(b0 + off + 1024);
+                    }
+#pragma unroll
+                    for (int i = 0; i < FM; ++i) {
+                        if constexpr (OP == OP_BASE) {
+                            acc[0][j][i] = mma<false>(bh, ah[i], acc[0][j][i]);
+                        } else if constexpr (OP == OP_FULL) {
+                            // head product, then the shifted residual product
+                            acc[0][j][i] = mma<false>(bh, ah[i], acc[0][j][i]);
+                            acc[1][j][i] = mma<false>(bh, al[i], acc[1][j][i]);
+                        } else if constexpr (OP == OP_SCORES) {
+                            // hiQ*hiK, hiQ*loK, loQ*hiK, loQ*loK
+                            acc[0][j][i] = mma<false>(bh, ah[i], acc[0][j][i]);
+                            acc[0][j][i] = mma<false>(bl, ah[i], acc[0][j][i]);
+                            acc[0][j][i] = mma<false>(bh, al[i], acc[0][j][i]);
+                            acc[0][j][i] = mma<false>(bl, al[i], acc[0][j][i]);
+                        } else {
+                            // hiA*hiB, hiA*loB, loA*hiB: the order of heal_gemm_f32
+                            acc[0][j][i] = mma<true>(bh, ah[i], acc[0][j][i]);
+                            acc[0][j][i] = mma<true>(bl, ah[i], acc[0][j][i]);
+                            acc[0][j][i] = mma<true>(bh, al[i], acc[0][j][i]);
+                        }
+                    }
+                }
+            }
+        };
+
+        // ---- main loop: two LDS stages, one barrier per stage -------------
+        auto step = [&](const char *cur, char *nxt, int64_t kt) {
+            if (kt + 1 < nk) load_stage((kt + 1) * BK);
+            compute_stage(cur);
+            if (kt + 1 < nk) store_stage(nxt);
+            __syncthreads();
+        };
+        if (nk > 0) {
+            load_stage(0);
+            store_stage(smem0);
+            __syncthreads();
+        }
+        for (int64_t kt = 0; kt < nk; kt += 2) {
+            step(smem0, smem1, kt);
+            if (kt + 1 < nk) step(smem1, smem0, kt + 1);
+        }
+
+        // ---- epilogue: FP32 accumulators -> FP32 C, no downcast -----------
+        float factor = 1.0f;
+        if constexpr (OP == OP_SCORES) {
+            const float sq = *p.maxA / 32767.0f, sk = *p.maxB / 32767.0f;
+            const float prod = sq * sk;
+            factor = prod * p.alpha;
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int64_t m = m0 + wm * WM + i * 16 + fr;
+                const int64_t n = n0 + wn * WN + j * 16 + 4 * fg;
+                f32x4 v;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    if constexpr (OP == OP_BASE)
+                        v[t] = ldexpf(acc[0][j][i][t], -p.e);
+                    else if constexpr (OP == OP_FULL)
+                        v[t] = ldexpf(__builtin_fmaf(acc[1][j][i][t], 0x1p-10f, acc[0][j][i][t]),
+                                      -p.e);
+                    else if constexpr (OP == OP_SCORES)
+                        v[t] = acc[0][j][i][t] * factor;
+                    else
+                        v[t] = acc[0][j][i][t];
+                }
+                if (m < M && n < N) {
+                    float *cp = C + m * p.ldc + n;
+                    if (p.vecC && n + 4 <= N) {
+                        *reinterpret_cast<f32x4 *>(cp) = v;
+                    } else {
+                        cp[0] = v.x;
+                        if (n + 1 < N) cp[1] = v.y;
+                        if (n + 2 < N) cp[2] = v.z;
+                        if (n + 3 < N) cp[3] = v.w;
+                    }
+                }
+            }
+        }
+        if (b + gridDim.y < p.batch) __syncthreads();  // LDS reuse by the next batch entry
+    }
+}
+
+// Whether the 16-byte buffer-load path can run the call: rows aligned, whole
+// 16-byte units along K, and every byte offset inside a tile below 2^31.
+// (Packed B is always read with buffer loads; the caller bounds K so that a
+// tile's packed offsets stay below 2^31.)
+template <int OP, int BM, int BN, int BK>
+bool vec_path_applies(const OpArgs &a)
+{
+    using O = OpT<OP>;
+    const int64_t lim = 0x7fffffffLL;
+    const int esz_a = O::A_I16 ? 2 : 4;
+    const int upk = O::A_I16 ? 8 : 4;
+    if (!a.vecA || a.K % upk != 0) return false;
+    if (((int64_t)(BM - 1) * a.lda + a.K + BK) * esz_a >= lim) return false;
+    if (O::B_ROWS) {
+        if (!a.vecB || a.K % 8 != 0) return false;
+        if (((int64_t)(BN - 1) * a.ldb + a.K + BK) * 2 >= lim) return false;
+    }
+    return true;
+}
+
+template <int OP, int BM, int BN, int WM, int WN, int NT, int BK>
+hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
+{
+    const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+    if (tiles > 0x7fffffffLL) return hipErrorInvalidValue;
+    const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
+    const dim3 grid((unsigned)tiles, gy);
+    if (vec_path_applies<OP, BM, BN, BK>(a))
+        hipLaunchKernelGGL((gemm_op_kernel<OP, BM, BN, WM, WN, NT, BK, true>), grid, dim3(NT), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((gemm_op_kernel<OP, BM, BN, WM, WN, NT, BK, false>), grid, dim3(NT),
+                           0, stream, a);
+    return hipGetLastError();
+}
+
+// Instance configurations: BM, BN, WM, WN, threads, BK.
+#ifndef HEAL_OP_LARGE_CFG
+#define HEAL_OP_LARGE_CFG 128, 256, 64, 64, 512, 32
+#endif
+#ifndef HEAL_OP_MEDIUM_CFG
+#define HEAL_OP_MEDIUM_CFG 128, 128, 64, 64, 256, 32
+#endif
+#ifndef HEAL_OP_SKINNY16_CFG
+#define HEAL_OP_SKINNY16_CFG 16, 256, 16, 64, 256, 64
+#endif
+#ifndef HEAL_OP_SKINNY32_CFG
+#define HEAL_OP_SKINNY32_CFG 32, 256, 32, 64, 256, 64
+#endif
+#ifndef HEAL_OP_SKINNY64_CFG
+#define HEAL_OP_SKINNY64_CFG 64, 256, 64, 64, 256, 32
+#endif
+
+template <int OP>
+hipError_t launch_op(int instance, const OpArgs &a, hipStream_t stream)
+{
+    switch (instance) {
+    case HEAL_INSTANCE_LARGE: return launch_cfg<OP, HEAL_OP_LARGE_CFG>(a, stream);
+    case HEAL_INSTANCE_MEDIUM: return launch_cfg<OP, HEAL_OP_MEDIUM_CFG>(a, stream);
+    case HEAL_INSTANCE_SKINNY:
+        if (a.M <= 16) return launch_cfg<OP, HEAL_OP_SKINNY16_CFG>(a, stream);
+        if (a.M <= 32) return launch_cfg<OP, HEAL_OP_SKINNY32_CFG>(a, stream);
+        return launch_cfg<OP, HEAL_OP_SKINNY64_CFG>(a, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_gemm_op(int op, int instance, const OpArgs &a, hipStream_t stream)
+{
+    if (instance == HEAL_INSTANCE_AUTO)
+        instance = a.M <= 64 ? HEAL_INSTANCE_SKINNY
+                   : a.M * a.N <= (int64_t)2048 * 2048 ? HEAL_INSTANCE_MEDIUM
+                                                       : HEAL_INSTANCE_LARGE;
+    switch (op) {
+    case OP_BASE: return launch_op<OP_BASE>(instance, a, stream);
+    case OP_FULL: return launch_op<OP_FULL>(instance, a, stream);
+    case OP_SCORES: return launch_op<OP_SCORES>(instance, a, stream);
+    case OP_PRESPLIT: return launch_op<OP_PRESPLIT>(instance, a, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace heal

@@ -40,4 +40,43 @@ hipError_t launch_gemm_skinny(const GemmArgs &args, bool trans_b, bool use_alpha
 
 hipError_t launch_split(const float *x, uint16_t *hi, uint16_t *lo, int64_t n, hipStream_t stream);
 
+// ---- FP16 / INT16 forms and the pre-split operand (heal_ops.hip, heal_gemm_op.hip) ----
+
+// The products of heal_gemm_op.hip.
+enum OpKind : int {
+    OP_BASE = 0,      // HEAL-Base: f16(A) * W16, A FP32, W16 packed FP16
+    OP_FULL = 1,      // HEAL-Full: (A_hi * W16) + 2^-10 (A_lo * W16)
+    OP_SCORES = 2,    // HEAL+ scores: dual-FP16 of INT16 Q and K, four products
+    OP_PRESPLIT = 3,  // bf16x3 with B pre-split and packed
+};
+
+// One strided-batched product of heal_gemm_op.hip; sizes in elements.
+struct OpArgs {
+    int64_t M, N, K;
+    const void *A;  // FP32 M x K (BASE, FULL, PRESPLIT) or INT16 M x K (SCORES)
+    int64_t lda, strideA;
+    const void *B;  // packed uint16 (BASE, FULL, PRESPLIT) or INT16 N x K rows (SCORES)
+    int64_t ldb, strideB;
+    float *C;
+    int64_t ldc, strideC;
+    int64_t batch;
+    int e;                      // BASE, FULL: C is scaled by 2^-e
+    const float *maxA, *maxB;   // SCORES: max|Q|, max|K| (device)
+    float alpha;                // SCORES
+    int vecA, vecB, vecC;       // 16-byte rows (pointer, leading dimension, batch stride)
+};
+
+// instance: HEAL_INSTANCE_* (AUTO chooses from M and N).
+hipError_t launch_gemm_op(int op, int instance, const OpArgs &args, hipStream_t stream);
+
+hipError_t launch_split_f16(const float *x, uint16_t *hi, uint16_t *lo, int64_t n,
+                            hipStream_t stream);
+// kind 0: FP16 weight RNE_f16(src * 2^e), one plane; kind 1: bf16 (hi, lo) planes.
+hipError_t launch_pack(int kind, const float *src, int64_t K, int64_t N, int64_t ld, bool trans,
+                       int e, uint16_t *out, hipStream_t stream);
+hipError_t launch_maxabs(const float *x, int64_t rows, int64_t cols, int64_t ld, float *maxabs,
+                         hipStream_t stream);
+hipError_t launch_quantize(const float *x, int64_t n, int16_t *q, float *maxabs,
+                           hipStream_t stream);
+
 }  // namespace heal
