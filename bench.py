@@ -25,7 +25,21 @@ Prints ONE JSON line:
   cpu_baseline the CPU oracle timed on a bounded row sample of the same product
   comparison   MI355X native FP32 GEMM (torch.matmul, TF32 off) on the same inputs
   bit_repro    every timed step's output bitwise equal to the first
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+
+--method selects the product (default bf16x3, the line above):
+  presplit    heal_gemm_f32_presplit: B split once into packed bf16 (hi, lo)
+              before the timed region; same MFMAs, bitwise equal results;
+  f16_full    heal_gemm_f16w, HEAL-Full: W = B^T packed to FP16 (scaled by
+              2^e) before the timed region, two FP16 products per chunk;
+  f16_base    heal_gemm_f16w, HEAL-Base: one FP16 product per chunk;
+  i16_scores  heal_scores_i16 on the attention workload: Q and K quantized to
+              INT16 before the timed region (as stored in the KV cache), four
+              FP16 products per chunk.
+For every method a step is one launch of its GEMM kernel over the workload;
+value is FP32-equivalent TFLOP/s (2*M*N*K*batch per step); the roofline uses
+the method's own MFMA flops and operand bytes.
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--method NAME] [--no-cpu]
 """
 import argparse
 import hashlib
@@ -50,7 +64,18 @@ KERNEL_NAMES = {1: "gemm_large8_kernel (256x256 tiles, 8 waves of 64x128)",
                 3: "gemm_skinny_kernel (column strips, M <= 64)"}
 KERNEL_SOURCES = {1: ["heal_gemm_large.hip", "heal_device.h", "heal_internal.h"],
                   2: ["heal_gemm.hip", "heal_device.h", "heal_internal.h"],
-                  3: ["heal_gemm_skinny.hip", "heal_device.h", "heal_internal.h"]}
+                  3: ["heal_gemm_skinny.hip", "heal_device.h", "heal_internal.h"],
+                  "op": ["heal_gemm_op.hip", "heal_device.h", "heal_internal.h"]}
+OP_INSTANCE_NAMES = {1: "large 128x256, 8 waves", 2: "medium 128x128, 4 waves",
+                     3: "skinny M<=64, 256-column tiles"}
+# MFMA products per 32-deep chunk and output block, and bytes per operand element
+METHODS = {
+    "bf16x3": {"products": 3, "a_bytes": 4, "b_bytes": 4, "dtype": "bf16x3-f32acc"},
+    "presplit": {"products": 3, "a_bytes": 4, "b_bytes": 4, "dtype": "bf16x3-f32acc"},
+    "f16_full": {"products": 2, "a_bytes": 4, "b_bytes": 2, "dtype": "f16x2-f32acc"},
+    "f16_base": {"products": 1, "a_bytes": 4, "b_bytes": 2, "dtype": "f16-f32acc"},
+    "i16_scores": {"products": 4, "a_bytes": 2, "b_bytes": 2, "dtype": "i16-dual-f16-f32acc"},
+}
 
 
 def parse():
@@ -59,6 +84,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="square8192")
+    ap.add_argument("--method", default="bf16x3", choices=sorted(METHODS))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU oracle sample")
@@ -69,7 +95,7 @@ def parse():
 
 
 def kernel_source_hash(instance):
-    """Hash of the sources of the kernel an instance launches."""
+    """Hash of the sources of the kernel an instance launches ("op": heal_gemm_op.hip)."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES[instance]:
         with open(os.path.join(ROOT, "paper_2606_21023_amd", "csrc", name), "rb") as f:
@@ -77,37 +103,53 @@ def kernel_source_hash(instance):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, instance):
-    """HBM bytes per launch from counters, if measured on the current kernel sources."""
+def measured_traffic(key, instance):
+    """HBM bytes per launch from counters, if measured on the current kernel sources.
+    key: the workload name (bf16x3) or "method:workload"."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     with open(TRAFFIC_FILE) as f:
         t = json.load(f)
-    e = t.get("workloads", {}).get(workload)
+    e = t.get("workloads", {}).get(key)
     if not e or e.get("kernel_source_sha") != kernel_source_hash(instance):
         return None
     return e["fetch_kib"] * 1024.0 * t["read_factor"] + e["write_kib"] * 1024.0 * t["write_factor"]
 
 
-def cpu_baseline(w, A, B, target_s):
-    """Time the CPU oracle on the first R rows of the product, R grown to ~target_s."""
+def cpu_baseline(w, A, B, target_s, method="bf16x3", extra=None):
+    """Time the CPU oracle of the method on the first R rows of the product, R
+    grown to ~target_s.  A is M x K; B is K x N (bf16x3, presplit), the N x K
+    weight (f16_*), or the N x K INT16 keys (i16_scores, A the INT16 queries)."""
     from oracle import oracle
     orc = oracle.default()
+    if method in ("bf16x3", "presplit"):
+        fn = lambda r: orc.gemm3(A[:r], B)
+        N, K = B.shape[1], B.shape[0]
+        what = "split of B included, FP64 accumulation"
+    elif method in ("f16_full", "f16_base"):
+        prods = METHODS[method]["products"]
+        fn = lambda r: orc.gemm_f16w(A[:r], B, extra["e"], prods)
+        N, K = B.shape
+        what = "FP16 weight cast included, FP64 accumulation"
+    else:
+        fn = lambda r: orc.scores_i16(A[:r], B, extra["maxQ"], extra["maxK"], w.alpha)
+        N, K = B.shape
+        what = "dual-FP16 unpack included, FP64 accumulation"
     rows = 1
     while True:
         t0 = time.perf_counter()
-        orc.gemm3(A[:rows], B)
+        fn(rows)
         t = time.perf_counter() - t0
         if t >= target_s or rows >= A.shape[0]:
             break
         grow = max(2, int(target_s / max(t, 1e-3)))
         rows = min(A.shape[0], rows * grow)
-    flops = 2.0 * rows * B.shape[1] * B.shape[0]
+    flops = 2.0 * rows * N * K
     return {"value": round(flops / t / 1e12, 5), "unit": "TFLOP/s", "cores": orc.num_threads(),
             "kind": "oracle", "seconds": round(t, 3),
-            "sample": "first %d of %d rows of one %s product (%dx%dx%d of the %d-entry batch), "
-                      "split of B included, FP64 accumulation" % (
-                          rows, A.shape[0], w.name, rows, B.shape[1], B.shape[0], w.batch)}
+            "sample": "%s oracle: first %d of %d rows of one %s product (%dx%dx%d of the "
+                      "%d-entry batch), %s" % (method, rows, A.shape[0], w.name, rows, N, K,
+                                                w.batch, what)}
 
 
 def main():
@@ -122,31 +164,86 @@ def main():
     import paper_2606_21023_amd as heal
     from paper_2606_21023_amd import workloads as wl
 
+    method = args.method
     w = wl.WORKLOADS[args.workload]
+    if method == "i16_scores" and w.name != "attn_scores":
+        print("--method i16_scores runs on the attn_scores workload", file=sys.stderr)
+        sys.exit(2)
+    if method in ("presplit", "f16_full", "f16_base") and (w.batch > 1 or w.trans_b):
+        print("--method %s runs on the linear-layer workloads" % method, file=sys.stderr)
+        sys.exit(2)
     A, B = wl.make_inputs(w)
     torch.cuda.init()
     dev = torch.device("cuda:0")
     batched = w.trans_b or w.batch > 1
+    meta = METHODS[method]
+
+    # Operand preparation outside the timed region (done once per weight or
+    # cache entry in use): FP16 weight packing, B pre-split, INT16 codes.
+    extra = {}
+    if method in ("f16_full", "f16_base"):
+        Wh = np.ascontiguousarray(B.T)            # the N x K weight of a linear layer
+        extra["e"] = heal.heal_f16_weight_exponent(float(np.abs(Wh).max()))
+    if method == "i16_scores":
+        q, mq = heal.heal_quantize_i16(torch.from_numpy(A).to(dev))
+        k, mk = heal.heal_quantize_i16(torch.from_numpy(B).to(dev))
+        torch.cuda.synchronize()
+        Aq, Bq = q.cpu().numpy(), k.cpu().numpy()
+        extra["maxQ"], extra["maxK"] = float(mq.item()), float(mk.item())
+
+    # algorithmic bytes per launch: A and B read once in the method's storage
+    # format, C written once in FP32
+    b_elems = w.K * w.N
+    if method in ("presplit", "f16_full", "f16_base"):
+        planes = 2 if method == "presplit" else 1
+        b_elems = heal.heal_packed_size(w.K, w.N, planes) // planes   # padded to 16 x 32 blocks
+    alg_bytes = float(w.batch) * (meta["a_bytes"] * w.M * w.K + meta["b_bytes"] * b_elems +
+                                  4.0 * w.M * w.N)
+
     # Rotate through copies of the operands so that HBM-bound shapes are not
     # served from the 256 MB Infinity Cache: at least 1 GiB of inputs in turn.
-    n_rot = int(min(16, max(1, math.ceil(float(1 << 30) / w.algorithmic_bytes))))
+    n_rot = int(min(16, max(1, math.ceil(float(1 << 30) / alg_bytes))))
     sets = []
     for _ in range(n_rot):
-        Ad = torch.from_numpy(A).to(dev)
-        Bd = torch.from_numpy(B).to(dev)
         shape = (w.batch, w.M, w.N) if batched else (w.M, w.N)
-        sets.append((Ad, Bd, torch.empty(shape, dtype=torch.float32, device=dev)))
+        Cd = torch.empty(shape, dtype=torch.float32, device=dev)
+        if method == "i16_scores":
+            Ad, Bd = torch.from_numpy(Aq).to(dev), torch.from_numpy(Bq).to(dev)
+            sets.append((Ad, Bd, Cd, mq.clone(), mk.clone()))
+            continue
+        Ad = torch.from_numpy(A).to(dev)
+        if method in ("f16_full", "f16_base"):
+            Bd = heal.heal_pack_f16_weight(torch.from_numpy(Wh).to(dev), extra["e"])
+        elif method == "presplit":
+            Bd = heal.heal_presplit_b(torch.from_numpy(B).to(dev))
+        else:
+            Bd = torch.from_numpy(B).to(dev)
+        sets.append((Ad, Bd, Cd))
+    torch.cuda.synchronize()
 
     # Launch through the C ABI with pre-built arguments, so that the timed
     # loop measures the kernels rather than argument marshalling: every step
-    # is one heal_gemm_f32 (or strided-batched) call on the current stream.
+    # is one library call on the current stream.
     import ctypes
     L = heal.lib()
     stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
     calls = []
-    for Ad, Bd, Cd in sets:
-        if batched:
+    for st in sets:
+        Ad, Bd, Cd = st[0], st[1], st[2]
+        if method == "i16_scores":
+            cargs = (w.M, w.N, w.K, Ad.data_ptr(), w.K, w.M * w.K, st[3].data_ptr(), Bd.data_ptr(),
+                     w.K, w.N * w.K, st[4].data_ptr(), ctypes.c_float(w.alpha), Cd.data_ptr(),
+                     w.N, w.M * w.N, w.batch, sp)
+            calls.append((L.heal_scores_i16, cargs))
+        elif method in ("f16_full", "f16_base"):
+            cargs = (meta["products"], w.M, w.N, w.K, Ad.data_ptr(), w.K, Bd.data_ptr(),
+                     extra["e"], Cd.data_ptr(), w.N, sp)
+            calls.append((L.heal_gemm_f16w, cargs))
+        elif method == "presplit":
+            cargs = (w.M, w.N, w.K, Ad.data_ptr(), w.K, Bd.data_ptr(), Cd.data_ptr(), w.N, sp)
+            calls.append((L.heal_gemm_f32_presplit, cargs))
+        elif batched:
             lda, ldb, ldc = w.K, (w.K if w.trans_b else w.N), w.N
             cargs = (w.M, w.N, w.K, ctypes.c_float(w.alpha), Ad.data_ptr(), lda, w.M * w.K,
                      Bd.data_ptr(), ldb, w.N * w.K, 1 if w.trans_b else 0, Cd.data_ptr(), ldc,
@@ -188,31 +285,39 @@ def main():
 
     flops = w.flops
     value = flops / (ms_per_step * 1e-3) / 1e12
-    mfma_flops = 3.0 * flops
+    mfma_flops = meta["products"] * flops
     t_mfma = mfma_flops / (BF16_DENSE_PEAK_TFLOPS * 1e12)
-    t_hbm = w.algorithmic_bytes / (HBM_PEAK_GBS * 1e9)
+    t_hbm = alg_bytes / (HBM_PEAK_GBS * 1e9)
     instance = heal.select_instance(w.M, w.N)
-    traffic = measured_traffic(w.name, instance)
+    if method == "bf16x3":
+        traffic = measured_traffic(w.name, instance)
+        kernel = KERNEL_NAMES.get(instance, "?")
+    else:
+        traffic = measured_traffic("%s:%s" % (method, w.name), "op")
+        kernel = "gemm_op_kernel<%s> (%s)" % (method, OP_INSTANCE_NAMES.get(instance, "?"))
+    mfma_dtype = "bf16" if meta["products"] == 3 else "f16"
     if t_mfma >= t_hbm:
         achieved = mfma_flops / (avg_launch_ms * 1e-3) / 1e12
         roofline = {"bound": "mfma", "achieved": round(achieved, 2),
                     "peak": BF16_DENSE_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": round(achieved / BF16_DENSE_PEAK_TFLOPS, 4)}
-        per_launch = "6*M*N*K*batch bf16 MFMA flops = %.4g" % mfma_flops
+        per_launch = "%d*2*M*N*K*batch %s MFMA flops = %.4g" % (meta["products"], mfma_dtype,
+                                                               mfma_flops)
     else:
-        achieved = w.algorithmic_bytes / (avg_launch_ms * 1e-3) / 1e9
+        achieved = alg_bytes / (avg_launch_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
-        per_launch = "4*(M*K + K*N + M*N)*batch bytes = %.4g" % w.algorithmic_bytes
+        per_launch = ("(%d*M*K + %d*K*N + 4*M*N)*batch bytes = %.4g"
+                      % (meta["a_bytes"], meta["b_bytes"], alg_bytes))
     roofline.update({"traffic": None if traffic is None else round(traffic),
-                     "kernel": KERNEL_NAMES.get(instance, "?"),
-                     "per_launch": per_launch, "avg_launch_us": round(avg_launch_ms * 1e3, 2)})
+                     "kernel": kernel, "per_launch": per_launch,
+                     "avg_launch_us": round(avg_launch_ms * 1e3, 2)})
 
-    # MI355X native FP32 GEMM on the same inputs, TF32 off
+    # MI355X native FP32 GEMM on the same (FP32) inputs, TF32 off
     torch.backends.cuda.matmul.allow_tf32 = False
     torch.set_float32_matmul_precision("highest")
-    Ad, Bd, _ = sets[0]
-    mm = (lambda: torch.matmul(Ad, Bd.transpose(-1, -2))) if w.trans_b else (lambda: Ad @ Bd)
+    Af, Bf = torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
+    mm = (lambda: torch.matmul(Af, Bf.transpose(-1, -2))) if w.trans_b else (lambda: Af @ Bf)
     for _ in range(3):
         mm()
     torch.cuda.synchronize()
@@ -226,15 +331,24 @@ def main():
     native_ms = e0.elapsed_time(e1) / reps
     comparison = {"torch_fp32_matmul_tflops": round(flops / (native_ms * 1e-3) / 1e12, 2),
                   "torch_fp32_matmul_ms": round(native_ms, 4)}
+    del Af, Bf
 
     cpu = None
     if not args.no_cpu:
-        Ah = A[0] if batched else A
-        Bh = np.ascontiguousarray(B[0].T) if w.trans_b else (B[0] if batched else B)
-        cpu = cpu_baseline(w, Ah, Bh, args.cpu_seconds)
+        if method == "i16_scores":
+            cpu = cpu_baseline(w, Aq[0], Bq[0], args.cpu_seconds, method, extra)
+        elif method in ("f16_full", "f16_base"):
+            cpu = cpu_baseline(w, A, Wh, args.cpu_seconds, method, extra)
+        else:
+            Ah = A[0] if batched else A
+            Bh = np.ascontiguousarray(B[0].T) if w.trans_b else (B[0] if batched else B)
+            cpu = cpu_baseline(w, Ah, Bh, args.cpu_seconds, method, extra)
 
+    names = {"bf16x3": "compensated GEMM", "presplit": "compensated GEMM, pre-split B",
+             "f16_full": "HEAL-Full FP16 GEMM", "f16_base": "HEAL-Base FP16 GEMM",
+             "i16_scores": "INT16 dual-FP16 attention scores"}
     line = {
-        "metric": "FP32-equiv TFLOP/s of compensated GEMM; % of bf16 MFMA peak/3; bit-repro",
+        "metric": "FP32-equiv TFLOP/s of %s; %% of bf16 MFMA peak/3; bit-repro" % names[method],
         "value": round(value, 2),
         "unit": "TFLOP/s (FP32-equivalent, 2MNK/t)",
         "n_gpus": 1,
@@ -244,19 +358,21 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16x3-f32acc",
+        "dtype": meta["dtype"],
         "data": "synthetic",
-        "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "batch": w.batch,
-                   "trans_b": w.trans_b, "alpha": w.alpha, "seed": w.seed,
+        "config": {"workload": w.name, "method": method, "M": w.M, "N": w.N, "K": w.K,
+                   "batch": w.batch, "trans_b": w.trans_b, "alpha": w.alpha, "seed": w.seed,
                    "inputs": w.note, "operand_copies_rotated": n_rot},
         "pct_of_bf16_peak_div3": round(100.0 * value / (BF16_DENSE_PEAK_TFLOPS / 3), 2),
-        "hbm_gbs": round(w.algorithmic_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "hbm_gbs": round(alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "bit_repro": {"runs": args.steps + args.warmup + 1, "identical": identical},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "comparison": comparison,
         "wall_s": round(wall, 3),
     }
+    if "e" in extra:
+        line["config"]["weight_exponent"] = extra["e"]
     print(json.dumps(line))
     sys.stdout.flush()
 

@@ -109,9 +109,12 @@ gemm_op_kernel(OpArgs p)
     constexpr int STAGE = O::AP * A_PLANE + O::BP * B_PLANE;
     constexpr int WAVES_M = BM / WM;
     constexpr int FM = WM / 16, FN = WN / 16;
-    static_assert(BK % 32 == 0 && BK <= 128, "stage depth");
+    // the first CWAVES waves compute one wave tile each; all NT threads load
+    // and convert (extra waves only help move a narrow tile's operands)
+    constexpr int CWAVES = WAVES_M * (BN / WN);
+    static_assert(BK % 32 == 0 && BK <= 256, "stage depth");
     static_assert(BM % WM == 0 && BN % WN == 0 && WM % 16 == 0 && WN % 16 == 0, "wave tiling");
-    static_assert(WAVES_M * (BN / WN) * 64 == NT, "every wave computes one wave tile");
+    static_assert(CWAVES * 64 <= NT && NT % 64 == 0, "compute waves exceed the workgroup");
 
     // 16-byte load units of one stage
     constexpr int A_EPU = O::A_I16 ? 8 : 4;      // A elements per unit
@@ -133,7 +136,8 @@ gemm_op_kernel(OpArgs p)
     const int fr = lane & 15;
     const int fg = lane >> 4;
     const int wm = wave % WAVES_M;
-    const int wn = wave / WAVES_M;
+    const int wn = (wave / WAVES_M) % (BN / WN);
+    const bool computes = CWAVES * 64 == NT || wave < CWAVES;
 
     auto swz = [](int row) { return (row / RPW) & SWM; };
     auto chunk_off = [&](int row, int c) { return row * ROWB + ((c ^ swz(row)) << 4); };
@@ -384,7 +388,7 @@ gemm_op_kernel(OpArgs p)
         // ---- main loop: two LDS stages, one barrier per stage -------------
         auto step = [&](const char *cur, char *nxt, int64_t kt) {
             if (kt + 1 < nk) load_stage((kt + 1) * BK);
-            compute_stage(cur);
+            if (computes) compute_stage(cur);
             if (kt + 1 < nk) store_stage(nxt);
             __syncthreads();
         };
@@ -409,6 +413,7 @@ gemm_op_kernel(OpArgs p)
         for (int j = 0; j < FN; ++j) {
 #pragma unroll
             for (int i = 0; i < FM; ++i) {
+                if (!computes) break;
                 const int64_t m = m0 + wm * WM + i * 16 + fr;
                 const int64_t n = n0 + wn * WN + j * 16 + 4 * fg;
                 f32x4 v;
@@ -477,13 +482,27 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
     return hipGetLastError();
 }
 
-// Instance configurations: BM, BN, WM, WN, threads, BK.
+// Instance configurations: BM, BN, WM, WN, threads, BK.  Threads beyond the
+// (BM/WM)(BN/WN) compute waves only load and convert.  HEAL-Full keeps two
+// accumulators per block, so its waves own 64 x 64 (128 accumulator VGPRs at
+// two waves per SIMD).
 #ifndef HEAL_OP_LARGE_CFG
 #define HEAL_OP_LARGE_CFG 128, 256, 64, 64, 512, 32
+#endif
+#ifndef HEAL_OP_LARGE_FULL_CFG
+#define HEAL_OP_LARGE_FULL_CFG HEAL_OP_LARGE_CFG
+#endif
+// one accumulator per block: 256 x 256 tiles, eight waves of 64 x 128
+#ifndef HEAL_OP_LARGE_BASE_CFG
+#define HEAL_OP_LARGE_BASE_CFG 256, 256, 64, 128, 512, 64
+#endif
+#ifndef HEAL_OP_LARGE_PRESPLIT_CFG
+#define HEAL_OP_LARGE_PRESPLIT_CFG 256, 256, 64, 128, 512, 32
 #endif
 #ifndef HEAL_OP_MEDIUM_CFG
 #define HEAL_OP_MEDIUM_CFG 128, 128, 64, 64, 256, 32
 #endif
+// M <= 64, wide N: 256-column tiles, four compute waves of 16..64 x 64
 #ifndef HEAL_OP_SKINNY16_CFG
 #define HEAL_OP_SKINNY16_CFG 16, 256, 16, 64, 256, 64
 #endif
@@ -493,17 +512,49 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 #ifndef HEAL_OP_SKINNY64_CFG
 #define HEAL_OP_SKINNY64_CFG 64, 256, 64, 64, 256, 32
 #endif
+// M <= 64, narrow N (too few 256-column tiles to fill the chip): 16-column
+// tiles, one compute wave, three more waves that load and convert
+#ifndef HEAL_OP_NARROW16_CFG
+#define HEAL_OP_NARROW16_CFG 16, 16, 16, 16, 256, 256
+#endif
+#ifndef HEAL_OP_NARROW32_CFG
+#define HEAL_OP_NARROW32_CFG 32, 16, 32, 16, 256, 128
+#endif
+#ifndef HEAL_OP_NARROW64_CFG
+#define HEAL_OP_NARROW64_CFG 64, 16, 64, 16, 256, 64
+#endif
+// 256-column tiles are used while they number at least this many
+#ifndef HEAL_OP_WIDE_MIN_TILES
+#define HEAL_OP_WIDE_MIN_TILES 384
+#endif
+
+template <int OP>
+hipError_t launch_large(const OpArgs &a, hipStream_t stream)
+{
+    if constexpr (OP == OP_FULL) return launch_cfg<OP, HEAL_OP_LARGE_FULL_CFG>(a, stream);
+    else if constexpr (OP == OP_BASE) return launch_cfg<OP, HEAL_OP_LARGE_BASE_CFG>(a, stream);
+    else if constexpr (OP == OP_PRESPLIT)
+        return launch_cfg<OP, HEAL_OP_LARGE_PRESPLIT_CFG>(a, stream);
+    else return launch_cfg<OP, HEAL_OP_LARGE_CFG>(a, stream);
+}
 
 template <int OP>
 hipError_t launch_op(int instance, const OpArgs &a, hipStream_t stream)
 {
     switch (instance) {
-    case HEAL_INSTANCE_LARGE: return launch_cfg<OP, HEAL_OP_LARGE_CFG>(a, stream);
+    case HEAL_INSTANCE_LARGE: return launch_large<OP>(a, stream);
     case HEAL_INSTANCE_MEDIUM: return launch_cfg<OP, HEAL_OP_MEDIUM_CFG>(a, stream);
-    case HEAL_INSTANCE_SKINNY:
-        if (a.M <= 16) return launch_cfg<OP, HEAL_OP_SKINNY16_CFG>(a, stream);
-        if (a.M <= 32) return launch_cfg<OP, HEAL_OP_SKINNY32_CFG>(a, stream);
-        return launch_cfg<OP, HEAL_OP_SKINNY64_CFG>(a, stream);
+    case HEAL_INSTANCE_SKINNY: {
+        const bool wide = (a.N + 255) / 256 >= HEAL_OP_WIDE_MIN_TILES;
+        if (a.M <= 16)
+            return wide ? launch_cfg<OP, HEAL_OP_SKINNY16_CFG>(a, stream)
+                        : launch_cfg<OP, HEAL_OP_NARROW16_CFG>(a, stream);
+        if (a.M <= 32)
+            return wide ? launch_cfg<OP, HEAL_OP_SKINNY32_CFG>(a, stream)
+                        : launch_cfg<OP, HEAL_OP_NARROW32_CFG>(a, stream);
+        return wide ? launch_cfg<OP, HEAL_OP_SKINNY64_CFG>(a, stream)
+                    : launch_cfg<OP, HEAL_OP_NARROW64_CFG>(a, stream);
+    }
     default: return hipErrorInvalidValue;
     }
 }
