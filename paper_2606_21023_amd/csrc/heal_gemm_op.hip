@@ -538,6 +538,12 @@ hipError_t launch_large(const OpArgs &a, hipStream_t stream)
     else return launch_cfg<OP, HEAL_OP_LARGE_CFG>(a, stream);
 }
 
+// HEAL-Full at M <= 64, wide N: eight waves of 64 x 32, so that the two
+// accumulators fit two waves per SIMD
+#ifndef HEAL_OP_SKINNY64_FULL_CFG
+#define HEAL_OP_SKINNY64_FULL_CFG 64, 256, 64, 32, 512, 32
+#endif
+
 template <int OP>
 hipError_t launch_op(int instance, const OpArgs &a, hipStream_t stream)
 {
@@ -552,8 +558,9 @@ hipError_t launch_op(int instance, const OpArgs &a, hipStream_t stream)
         if (a.M <= 32)
             return wide ? launch_cfg<OP, HEAL_OP_SKINNY32_CFG>(a, stream)
                         : launch_cfg<OP, HEAL_OP_NARROW32_CFG>(a, stream);
-        return wide ? launch_cfg<OP, HEAL_OP_SKINNY64_CFG>(a, stream)
-                    : launch_cfg<OP, HEAL_OP_NARROW64_CFG>(a, stream);
+        if (!wide) return launch_cfg<OP, HEAL_OP_NARROW64_CFG>(a, stream);
+        if constexpr (OP == OP_FULL) return launch_cfg<OP, HEAL_OP_SKINNY64_FULL_CFG>(a, stream);
+        return launch_cfg<OP, HEAL_OP_SKINNY64_CFG>(a, stream);
     }
     default: return hipErrorInvalidValue;
     }
