@@ -7,9 +7,13 @@
 //               C = 2^-e * sum_k f16(a) w16.
 //   OP_FULL     HEAL-Full (Section 4, GEMM paragraph and its two-product
 //               expansion): the activation is the pair h_hi = f16(h),
-//               h_lo = f16((h - h_hi) 2^10); two products into two FP32
-//               accumulators, combined once at the end:
-//               C = 2^-e * (acc_hi + 2^-10 acc_lo).
+//               h_lo = f16((h - h_hi) 2^10); both products go into one FP32
+//               accumulator, the residual's 2^-10 moved onto the weight
+//               (GEMM(h_lo / 2^10, W) = GEMM(h_lo, W / 2^10)):
+//               C = 2^-e * sum_k (h_hi w16 + h_lo f16(w16 2^-10)).
+//               w16 2^-10 is exact for |w16| >= 2^-4, i.e. every weight
+//               above 2^-20 of the largest one (the scaled weights reach
+//               2^15).
 //   OP_SCORES   HEAL+ score product (Section 4, Q/K/V paragraph and its
 //               attention expansion): INT16 codes of Q and K are unpacked into
 //               dual-FP16 pairs and all four products are accumulated:
@@ -46,26 +50,26 @@ namespace {
 
 template <int OP>
 struct OpT;
-// AP, BP: LDS planes of A and B; NACC: accumulators per output block;
+// AP, BP: LDS planes of A and B;
 // A_I16: A holds INT16 codes; B_ROWS: B is INT16 N x K rows (else packed).
 template <>
 struct OpT<OP_BASE> {
-    static constexpr int AP = 1, BP = 1, NACC = 1;
+    static constexpr int AP = 1, BP = 1;
     static constexpr bool A_I16 = false, B_ROWS = false;
 };
 template <>
 struct OpT<OP_FULL> {
-    static constexpr int AP = 2, BP = 1, NACC = 2;
+    static constexpr int AP = 2, BP = 1;
     static constexpr bool A_I16 = false, B_ROWS = false;
 };
 template <>
 struct OpT<OP_SCORES> {
-    static constexpr int AP = 2, BP = 2, NACC = 1;
+    static constexpr int AP = 2, BP = 2;
     static constexpr bool A_I16 = true, B_ROWS = true;
 };
 template <>
 struct OpT<OP_PRESPLIT> {
-    static constexpr int AP = 2, BP = 2, NACC = 1;
+    static constexpr int AP = 2, BP = 2;
     static constexpr bool A_I16 = false, B_ROWS = false;
 };
 
@@ -177,13 +181,11 @@ gemm_op_kernel(OpArgs p)
             O::B_ROWS ? make_rsrc(Bb + n0 * p.ldb * 2)
                       : make_rsrc(Bb + (n0 / 16) * KC * O::BP * 1024);
 
-        f32x4 acc[O::NACC][FN][FM];
+        f32x4 acc[FN][FM];
 #pragma unroll
-        for (int a = 0; a < O::NACC; ++a)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-#pragma unroll
-                for (int i = 0; i < FM; ++i) acc[a][j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int i = 0; i < FM; ++i) acc[j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
         u32x4 ra[A_IT], rb[B_IT];
 
@@ -360,25 +362,32 @@ gemm_op_kernel(OpArgs p)
                         bh = *reinterpret_cast<const u32x4 *>(b0 + off);
                         if (O::BP == 2) bl = *reinterpret_cast<const u32x4 *>(b0 + off + 1024);
                     }
+                    // HEAL-Full: the weight fragment scaled by 2^-10 for the
+                    // residual product (exact unless it lands below 2^-14)
+                    u32x4 bs;
+                    if constexpr (OP == OP_FULL)
+                        bs = __builtin_bit_cast(
+                            u32x4, __builtin_bit_cast(f16x8, bh) * (_Float16)0x1p-10f);
 #pragma unroll
                     for (int i = 0; i < FM; ++i) {
                         if constexpr (OP == OP_BASE) {
-                            acc[0][j][i] = mma<false>(bh, ah[i], acc[0][j][i]);
+                            acc[j][i] = mma<false>(bh, ah[i], acc[j][i]);
                         } else if constexpr (OP == OP_FULL) {
-                            // head product, then the shifted residual product
-                            acc[0][j][i] = mma<false>(bh, ah[i], acc[0][j][i]);
-                            acc[1][j][i] = mma<false>(bh, al[i], acc[1][j][i]);
+                            // head product, then the residual product with the
+                            // 2^-10 moved onto the weight: h_lo * (w 2^-10)
+                            acc[j][i] = mma<false>(bh, ah[i], acc[j][i]);
+                            acc[j][i] = mma<false>(bs, al[i], acc[j][i]);
                         } else if constexpr (OP == OP_SCORES) {
                             // hiQ*hiK, hiQ*loK, loQ*hiK, loQ*loK
-                            acc[0][j][i] = mma<false>(bh, ah[i], acc[0][j][i]);
-                            acc[0][j][i] = mma<false>(bl, ah[i], acc[0][j][i]);
-                            acc[0][j][i] = mma<false>(bh, al[i], acc[0][j][i]);
-                            acc[0][j][i] = mma<false>(bl, al[i], acc[0][j][i]);
+                            acc[j][i] = mma<false>(bh, ah[i], acc[j][i]);
+                            acc[j][i] = mma<false>(bl, ah[i], acc[j][i]);
+                            acc[j][i] = mma<false>(bh, al[i], acc[j][i]);
+                            acc[j][i] = mma<false>(bl, al[i], acc[j][i]);
                         } else {
                             // hiA*hiB, hiA*loB, loA*hiB: the order of heal_gemm_f32
-                            acc[0][j][i] = mma<true>(bh, ah[i], acc[0][j][i]);
-                            acc[0][j][i] = mma<true>(bl, ah[i], acc[0][j][i]);
-                            acc[0][j][i] = mma<true>(bh, al[i], acc[0][j][i]);
+                            acc[j][i] = mma<true>(bh, ah[i], acc[j][i]);
+                            acc[j][i] = mma<true>(bl, ah[i], acc[j][i]);
+                            acc[j][i] = mma<true>(bh, al[i], acc[j][i]);
                         }
                     }
                 }
@@ -419,15 +428,12 @@ gemm_op_kernel(OpArgs p)
                 f32x4 v;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    if constexpr (OP == OP_BASE)
-                        v[t] = ldexpf(acc[0][j][i][t], -p.e);
-                    else if constexpr (OP == OP_FULL)
-                        v[t] = ldexpf(__builtin_fmaf(acc[1][j][i][t], 0x1p-10f, acc[0][j][i][t]),
-                                      -p.e);
+                    if constexpr (OP == OP_BASE || OP == OP_FULL)
+                        v[t] = ldexpf(acc[j][i][t], -p.e);
                     else if constexpr (OP == OP_SCORES)
-                        v[t] = acc[0][j][i][t] * factor;
+                        v[t] = acc[j][i][t] * factor;
                     else
-                        v[t] = acc[0][j][i][t];
+                        v[t] = acc[j][i][t];
                 }
                 if (m < M && n < N) {
                     float *cp = C + m * p.ldc + n;
@@ -483,16 +489,15 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 }
 
 // Instance configurations: BM, BN, WM, WN, threads, BK.  Threads beyond the
-// (BM/WM)(BN/WN) compute waves only load and convert.  HEAL-Full keeps two
-// accumulators per block, so its waves own 64 x 64 (128 accumulator VGPRs at
-// two waves per SIMD).
+// (BM/WM)(BN/WN) compute waves only load and convert.
 #ifndef HEAL_OP_LARGE_CFG
 #define HEAL_OP_LARGE_CFG 128, 256, 64, 64, 512, 32
 #endif
+// 256 x 256 tiles, eight waves of 64 x 128 (128 accumulator VGPRs at two
+// waves per SIMD)
 #ifndef HEAL_OP_LARGE_FULL_CFG
-#define HEAL_OP_LARGE_FULL_CFG HEAL_OP_LARGE_CFG
+#define HEAL_OP_LARGE_FULL_CFG 256, 256, 64, 128, 512, 32
 #endif
-// one accumulator per block: 256 x 256 tiles, eight waves of 64 x 128
 #ifndef HEAL_OP_LARGE_BASE_CFG
 #define HEAL_OP_LARGE_BASE_CFG 256, 256, 64, 128, 512, 64
 #endif
@@ -538,8 +543,8 @@ hipError_t launch_large(const OpArgs &a, hipStream_t stream)
     else return launch_cfg<OP, HEAL_OP_LARGE_CFG>(a, stream);
 }
 
-// HEAL-Full at M <= 64, wide N: eight waves of 64 x 32, so that the two
-// accumulators fit two waves per SIMD
+// HEAL-Full at M <= 64, wide N: eight waves of 64 x 32 (measured faster than
+// four of 64 x 64: the A split is shared by twice the threads)
 #ifndef HEAL_OP_SKINNY64_FULL_CFG
 #define HEAL_OP_SKINNY64_FULL_CFG 64, 256, 64, 32, 512, 32
 #endif
