@@ -38,9 +38,9 @@ constexpr int kChunk = 32;  // K depth of one bf16 MFMA: the unit of the reducti
 #ifndef HEAL_SCHED_SPLIT_AT
 #define HEAL_SCHED_SPLIT_AT 4
 #endif
-// Large instance: BM, BN, BK, WM, WN, threads
+// Instance configurations: BM, BN, BK, WM, WN, threads
 #ifndef HEAL_MEDIUM_CFG
-#define HEAL_MEDIUM_CFG 128, 128, 32, 64, 64, 256
+#define HEAL_MEDIUM_CFG 128, 128, 32, 32, 64, 512
 #endif
 #ifndef HEAL_SKINNY16_CFG
 #define HEAL_SKINNY16_CFG 16, 64, 64, 16, 16, 256

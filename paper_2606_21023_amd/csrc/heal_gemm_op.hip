@@ -505,7 +505,7 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 #define HEAL_OP_LARGE_PRESPLIT_CFG 256, 256, 64, 128, 512, 32
 #endif
 #ifndef HEAL_OP_MEDIUM_CFG
-#define HEAL_OP_MEDIUM_CFG 128, 128, 64, 64, 256, 32
+#define HEAL_OP_MEDIUM_CFG 128, 128, 32, 64, 512, 32
 #endif
 // M <= 64, wide N: 256-column tiles, four compute waves of 16..64 x 64
 #ifndef HEAL_OP_SKINNY16_CFG
