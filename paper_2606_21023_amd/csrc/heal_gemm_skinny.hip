@@ -130,7 +130,17 @@ gemm_skinny_kernel(GemmArgs p)
     const int wave = tid >> 6;
     const int fr = lane & 15, fg = lane >> 4;
 
-    const int64_t n0 = (int64_t)blockIdx.x * BN;
+    // Strips are dealt to XCDs so that each XCD owns a contiguous run of
+    // them: workgroups are dispatched to the 8 XCDs round-robin, and without
+    // the renumbering two neighbouring 16-column strips, which read the two
+    // 64-byte halves of the same 128-byte lines of B, would each miss in a
+    // different XCD's L2 and fetch the line from HBM twice.
+    int64_t strip = blockIdx.x;
+    {
+        const int64_t nb = gridDim.x, x = strip & 7, i = strip >> 3, q = nb >> 3, r = nb & 7;
+        strip = x * q + (x < r ? x : r) + i;
+    }
+    const int64_t n0 = strip * BN;
     const int64_t M = p.M, N = p.N, K = p.K;
     const int cols = (int)((N - n0) < BN ? (N - n0) : BN);
     const int ns = (int)((K + BK - 1) / BK);
