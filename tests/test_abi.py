@@ -116,3 +116,68 @@ def test_binding_fails_loudly_without_library(monkeypatch):
     monkeypatch.setattr(heal, "library_path", "/nonexistent/libheal.so")
     with pytest.raises(heal.HealError):
         heal.lib()
+
+
+# ---- FP16 forms, pre-split operand, INT16 scores: validation without a GPU ----
+
+def _f16w(products=2, M=4, N=8, K=16, A=FAKE, lda=16, W=FAKE, e=0, C=FAKE, ldc=8, inst=0):
+    return heal.lib().heal_gemm_f16w_instance(inst, products, M, N, K, A, lda, W, e, C, ldc, None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(products=3), dict(products=0), dict(e=301), dict(e=-301), dict(M=-1), dict(K=-1),
+    dict(K=(1 << 20) + 4, lda=(1 << 20) + 4), dict(lda=15), dict(ldc=7), dict(A=0), dict(W=0),
+    dict(C=0), dict(A=FAKE + 2), dict(W=FAKE + 8), dict(C=FAKE + 1), dict(inst=17),
+])
+def test_gemm_f16w_rejects_invalid_arguments(kw):
+    assert _f16w(**kw) == INVALID
+
+
+def test_new_empty_calls_are_noops_without_device():
+    L = heal.lib()
+    assert _f16w(M=0, A=0, W=0, C=0) == 0
+    assert _f16w(N=0, A=0, W=0, C=0, ldc=1) == 0
+    assert L.heal_gemm_f32_presplit(0, 8, 16, 0, 16, 0, 0, 8, None) == 0
+    assert L.heal_pack_f16_weight(0, 0, 16, 16, 0, 0, None) == 0
+    assert L.heal_presplit_b(0, 16, 0, 1, 0, 0, None) == 0
+    assert L.heal_split_f16(0, 0, 0, 0, None) == 0
+    assert L.heal_scores_i16(0, 8, 16, 0, 16, 0, 0, 0, 16, 0, 0, ctypes.c_float(1.0), 0, 8, 0, 1,
+                             None) == 0
+
+
+def test_pack_and_presplit_reject_invalid_arguments():
+    L = heal.lib()
+    assert L.heal_pack_f16_weight(FAKE, 8, 16, 15, 0, FAKE, None) == INVALID      # ldw < K
+    assert L.heal_pack_f16_weight(FAKE, 8, 16, 16, 301, FAKE, None) == INVALID    # |e| > 300
+    assert L.heal_pack_f16_weight(FAKE, 8, 16, 16, 0, FAKE + 8, None) == INVALID  # W16 alignment
+    assert L.heal_pack_f16_weight(FAKE, -8, 16, 16, 0, FAKE, None) == INVALID
+    assert L.heal_presplit_b(FAKE, 16, 8, 8, 2, FAKE, None) == INVALID           # trans flag
+    assert L.heal_presplit_b(FAKE, 16, 8, 7, 0, FAKE, None) == INVALID           # ldb < N
+    assert L.heal_presplit_b(FAKE, 16, 8, 15, 1, FAKE, None) == INVALID          # ldb < K (N x K)
+    assert L.heal_presplit_b(FAKE, 16, 8, 8, 0, FAKE + 4, None) == INVALID       # Bp alignment
+    f = L.heal_gemm_f32_presplit
+    assert f(4, 8, 16, FAKE, 15, FAKE, FAKE, 8, None) == INVALID                  # lda < K
+    assert f(4, 8, 16, FAKE, 16, FAKE + 2, FAKE, 8, None) == INVALID              # Bp alignment
+    assert L.heal_gemm_f32_presplit_instance(9, 4, 8, 16, FAKE, 16, FAKE, FAKE, 8, None) == INVALID
+
+
+def test_scores_quantize_maxabs_split_f16_reject_invalid_arguments():
+    L = heal.lib()
+    one = ctypes.c_float(1.0)
+    s = L.heal_scores_i16
+    assert s(4, 8, 16, FAKE, 15, 0, FAKE, FAKE, 16, 0, FAKE, one, FAKE, 8, 0, 1, None) == INVALID
+    assert s(4, 8, 16, FAKE, 16, 0, FAKE, FAKE, 16, 0, FAKE, one, FAKE, 7, 0, 1, None) == INVALID
+    assert s(4, 8, 16, FAKE, 16, 0, 0, FAKE, 16, 0, FAKE, one, FAKE, 8, 0, 1, None) == INVALID
+    assert s(4, 8, 16, FAKE + 1, 16, 0, FAKE, FAKE, 16, 0, FAKE, one, FAKE, 8, 0, 1,
+             None) == INVALID
+    assert s(4, 8, 16, FAKE, 16, -1, FAKE, FAKE, 16, 0, FAKE, one, FAKE, 8, 0, 2, None) == INVALID
+    assert s(4, 8, 16, FAKE, 16, 0, FAKE, FAKE, 16, 0, FAKE, one, FAKE + 2, 8, 0, 1,
+             None) == INVALID
+    assert L.heal_quantize_i16(FAKE, -1, FAKE, FAKE, None) == INVALID
+    assert L.heal_quantize_i16(FAKE, 8, FAKE, 0, None) == INVALID
+    assert L.heal_quantize_i16(FAKE, 8, FAKE + 1, FAKE, None) == INVALID
+    assert L.heal_maxabs_f32(FAKE, 4, 8, 7, FAKE, None) == INVALID
+    assert L.heal_maxabs_f32(FAKE, 4, 8, 8, 0, None) == INVALID
+    assert L.heal_maxabs_f32(0, 4, 8, 8, FAKE, None) == INVALID
+    assert L.heal_split_f16(FAKE, FAKE, FAKE, -1, None) == INVALID
+    assert L.heal_split_f16(FAKE, FAKE + 1, FAKE, 8, None) == INVALID

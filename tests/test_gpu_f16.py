@@ -392,3 +392,45 @@ def test_scores_attention_workload(orc):
         S3 = heal.heal_scores_i16(q[:, :m].contiguous(), k, mq, mk, w.alpha)
         torch.cuda.synchronize()
         assert torch.equal(S3.view(torch.int32), S[:, :m].view(torch.int32)), "M=%d" % m
+
+
+@pytest.mark.parametrize("products", [1, 2], ids=["base", "full"])
+@pytest.mark.parametrize("instance", INSTANCES, ids=lambda i: INAME[i])
+def test_f16w_padded_and_misaligned(orc, products, instance):
+    """Leading dimensions above the width, A's base off 16 bytes (scalar load
+    path), C padded: the padding of C is untouched."""
+    M, N, K = 70, 90, 77
+    lda, ldc = K + 5, N + 7
+    rng = np.random.default_rng(6)
+    Abuf = (rng.standard_normal(M * lda + 1) * 2.0).astype(np.float32)
+    A = Abuf[1:].reshape(M, lda)[:, :K]
+    W = wl.random_matrix((N, K), seed=8, sigma=0.02)
+    e = heal.heal_f16_weight_exponent(float(np.abs(W).max()))
+    W16 = heal.heal_pack_f16_weight(to_dev(W), e)
+    Ad = torch.from_numpy(Abuf).cuda()[1:].view(M, lda)[:, :K]
+    Cbuf = torch.full((M * ldc + 1,), float("nan"), device="cuda")
+    Cd = Cbuf[1:].view(M, ldc)[:, :N]
+    announce("f16w padded/misaligned p%d %s" % (products, INAME[instance]))
+    heal.heal_gemm_f16w(Ad, W16, N, e, products, out=Cd, instance=instance)
+    torch.cuda.synchronize()
+    _, S = orc.gemm_f16w(np.ascontiguousarray(A), W, e, products)
+    check_tolerance(Cd.cpu().numpy(), S, f16w_absprod(orc, np.ascontiguousarray(A), W, e), "padded")
+    assert torch.isnan(Cbuf[1:].view(M, ldc)[:, N:]).all()
+
+
+def test_scores_padded_rows(orc):
+    """Q and K rows with leading dimensions above the head dimension (views
+    of wider buffers), batch strides of the views."""
+    bat, M, N, K = 2, 40, 50, 64
+    Qw, Kw = scores_case(bat, M, N, K + 8, seed=12)
+    Qv, Kv = to_dev(Qw)[:, :, :K], to_dev(Kw)[:, :, :K]
+    mq, mk = np.float32(1.25), np.float32(2.5)
+    announce("scores padded rows")
+    S = heal.heal_scores_i16(Qv, Kv, torch.tensor([mq], device="cuda"),
+                             torch.tensor([mk], device="cuda"), 0.5)
+    torch.cuda.synchronize()
+    f = factor(mq, mk, 0.5)
+    for b in range(bat):
+        Q, Kt = np.ascontiguousarray(Qw[b, :, :K]), np.ascontiguousarray(Kw[b, :, :K])
+        _, So = orc.scores_i16(Q, Kt, mq, mk, 0.5)
+        check_tolerance(S[b].cpu().numpy(), f * So, scores_absprod(Q, Kt, f), "padded b%d" % b)
