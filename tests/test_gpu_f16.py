@@ -434,3 +434,18 @@ def test_scores_padded_rows(orc):
         Q, Kt = np.ascontiguousarray(Qw[b, :, :K]), np.ascontiguousarray(Kw[b, :, :K])
         _, So = orc.scores_i16(Q, Kt, mq, mk, 0.5)
         check_tolerance(S[b].cpu().numpy(), f * So, scores_absprod(Q, Kt, f), "padded b%d" % b)
+
+
+def test_f16w_full_wide_weight_range(orc):
+    """HEAL-Full with weight columns spread over 2^-20 of the largest weight:
+    the residual product's weight fragment is scaled by 2^-10 in FP16, which
+    stays exact down to |w16| = 2^-4 and rounds below it, by at most 2^-25
+    per weight; the bars still hold over this range."""
+    M, N, K = 64, 96, 200
+    A = wl.random_matrix((M, K), seed=70, sigma=3.0)
+    W = wl.random_matrix((N, K), seed=71, sigma=0.05)
+    W *= np.exp2(-np.linspace(0.0, 20.0, N, dtype=np.float32))[:, None].astype(np.float32)
+    announce("f16w full, wide weight range")
+    C, e = run_f16w(A, W, 2)
+    _, S = orc.gemm_f16w(A, W, e, 2)
+    check_tolerance(C, S, f16w_absprod(orc, A, W, e), "wide weight range")
