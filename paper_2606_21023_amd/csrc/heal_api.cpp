@@ -33,6 +33,9 @@ heal_status_t check_device()
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
+// M x N outputs whose element count (and so every tile count) fits in 2^62.
+bool product_fits(int64_t M, int64_t N) { return M == 0 || N <= ((int64_t)1 << 62) / M; }
+
 int select_instance(int64_t M, int64_t N)
 {
     (void)N;
@@ -56,6 +59,7 @@ heal_status_t validate(int64_t M, int64_t N, int64_t K, const float *A, int64_t 
     const int64_t lim = (int64_t)1 << 48;
     if (M > lim || N > lim || K > lim || lda > lim || ldb > lim || ldc > lim || batch > lim)
         return HEAL_ERR_INVALID_VALUE;
+    if (!product_fits(M, N)) return HEAL_ERR_INVALID_VALUE;
     if (M == 0 || N == 0 || batch == 0) return HEAL_OK;
     if (!C || !aligned4(C)) return HEAL_ERR_INVALID_VALUE;
     if (K > 0 && (!A || !B || !aligned4(A) || !aligned4(B))) return HEAL_ERR_INVALID_VALUE;
@@ -116,6 +120,7 @@ heal_status_t run_packed(int op, int instance, int64_t M, int64_t N, int64_t K, 
     const int64_t lim = (int64_t)1 << 48;
     if (M > lim || N > ((int64_t)1 << 40) || lda > lim || ldc > lim) return HEAL_ERR_INVALID_VALUE;
     if (lda < (K > 1 ? K : 1) || ldc < (N > 1 ? N : 1)) return HEAL_ERR_INVALID_VALUE;
+    if (!product_fits(M, N)) return HEAL_ERR_INVALID_VALUE;
     if (instance < 0 || instance >= HEAL_INSTANCE_COUNT) return HEAL_ERR_INVALID_VALUE;
     if (M == 0 || N == 0) return HEAL_OK;
     if (!C || !aligned4(C)) return HEAL_ERR_INVALID_VALUE;
@@ -225,7 +230,8 @@ heal_status_t heal_maxabs_f32(const float *x, int64_t rows, int64_t cols, int64_
 {
     if (rows < 0 || cols < 0 || ld < (cols > 1 ? cols : 1) || !maxabs || !aligned4(maxabs))
         return HEAL_ERR_INVALID_VALUE;
-    if (rows > ((int64_t)1 << 40) || ld > ((int64_t)1 << 40)) return HEAL_ERR_INVALID_VALUE;
+    if (rows > ((int64_t)1 << 40) || ld > ((int64_t)1 << 40) || !product_fits(rows, ld))
+        return HEAL_ERR_INVALID_VALUE;
     if (rows > 0 && cols > 0 && (!x || !aligned4(x))) return HEAL_ERR_INVALID_VALUE;
     heal_status_t st = check_device();
     if (st != HEAL_OK) return st;
@@ -336,6 +342,7 @@ heal_status_t heal_scores_i16(int64_t M, int64_t N, int64_t K, const int16_t *Q,
     const int64_t lim = (int64_t)1 << 48;
     if (M > lim || N > lim || K > lim || ldq > lim || ldk > lim || lds > lim || batch > lim)
         return HEAL_ERR_INVALID_VALUE;
+    if (!product_fits(M, N)) return HEAL_ERR_INVALID_VALUE;
     if (M == 0 || N == 0 || batch == 0) return HEAL_OK;
     if (!S || !aligned4(S) || !maxQ || !maxK || !aligned4(maxQ) || !aligned4(maxK))
         return HEAL_ERR_INVALID_VALUE;

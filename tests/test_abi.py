@@ -181,3 +181,12 @@ def test_scores_quantize_maxabs_split_f16_reject_invalid_arguments():
     assert L.heal_maxabs_f32(0, 4, 8, 8, FAKE, None) == INVALID
     assert L.heal_split_f16(FAKE, FAKE, FAKE, -1, None) == INVALID
     assert L.heal_split_f16(FAKE, FAKE + 1, FAKE, 8, None) == INVALID
+
+
+def test_oversized_products_rejected():
+    """Outputs whose element count would overflow 64-bit tile arithmetic."""
+    L = heal.lib()
+    big = 1 << 40
+    assert L.heal_gemm_f32(big, big, 4, FAKE, FAKE, FAKE, 4, big, big, None) == INVALID
+    assert _f16w(M=big, N=1 << 39, ldc=1 << 39) == INVALID
+    assert L.heal_maxabs_f32(FAKE, 1 << 40, 8, 1 << 40, FAKE, None) == INVALID
