@@ -190,3 +190,23 @@ def test_oversized_products_rejected():
     assert L.heal_gemm_f32(big, big, 4, FAKE, FAKE, FAKE, 4, big, big, None) == INVALID
     assert _f16w(M=big, N=1 << 39, ldc=1 << 39) == INVALID
     assert L.heal_maxabs_f32(FAKE, 1 << 40, 8, 1 << 40, FAKE, None) == INVALID
+
+
+def test_header_is_plain_c_and_links(tmp_path):
+    """include/heal.h compiles as C11 with a plain C compiler, and a C program
+    linked against libheal.so sees the host-side contract (no GPU needed)."""
+    import shutil
+    import subprocess
+    from paper_2606_21023_amd import build as hbuild
+    gcc = shutil.which("gcc")
+    if gcc is None or not os.path.exists(hbuild.LIBRARY):
+        pytest.skip("gcc or libheal.so not available")
+    src = os.path.join(ROOT, "tests", "c", "abi_check.c")
+    exe = str(tmp_path / "abi_check")
+    libdir = os.path.dirname(hbuild.LIBRARY)
+    subprocess.run([gcc, "-std=c11", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                    "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include", src,
+                    "-L", libdir, "-lheal", "-Wl,-rpath," + libdir, "-o", exe], check=True)
+    r = subprocess.run([exe], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    assert "abi_check: ok" in r.stdout
