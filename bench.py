@@ -66,7 +66,7 @@ KERNEL_SOURCES = {1: ["heal_gemm_large.hip", "heal_device.h", "heal_internal.h"]
                   2: ["heal_gemm.hip", "heal_device.h", "heal_internal.h"],
                   3: ["heal_gemm_skinny.hip", "heal_device.h", "heal_internal.h"],
                   "op": ["heal_gemm_op.hip", "heal_device.h", "heal_internal.h"]}
-OP_INSTANCE_NAMES = {1: "large 256x256, 8 waves", 2: "medium 128x128, 8 waves",
+OP_INSTANCE_NAMES = {1: "large 128x256, 8 waves", 2: "medium 128x128, 8 waves",
                      3: "skinny M<=64, 256-column tiles"}
 # MFMA products per 32-deep chunk and output block, and bytes per operand element
 METHODS = {
@@ -81,8 +81,10 @@ METHODS = {
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    # about 0.2 s of warm-up at 8192^3: sub-millisecond launches reach their
+    # steady rate only after ~0.1-0.2 s of back-to-back work
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", default="square8192")
     ap.add_argument("--method", default="bf16x3", choices=sorted(METHODS))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -92,6 +94,15 @@ def parse():
                     help="after the timed region, copy a 1 GiB buffer 3 times (a plain copy "
                          "kernel of known size, for scaling HBM byte counters)")
     return ap.parse_args()
+
+
+def op_large_width(w, cus):
+    """Tile width the large FP16 / pre-split instance picks for workload w:
+    224 columns when that takes fewer rounds of one workgroup per CU."""
+    def cost(bn):
+        wgs = -(-w.M // 256) * -(-w.N // bn) * w.batch
+        return -(-wgs // cus) * bn
+    return 224 if cost(224) < cost(256) else 256
 
 
 def kernel_source_hash(instance):
@@ -294,7 +305,10 @@ def main():
         kernel = KERNEL_NAMES.get(instance, "?")
     else:
         traffic = measured_traffic("%s:%s" % (method, w.name), "op")
-        kernel = "gemm_op_kernel<%s> (%s)" % (method, OP_INSTANCE_NAMES.get(instance, "?"))
+        label = OP_INSTANCE_NAMES.get(instance, "?")
+        if instance == 1 and method != "i16_scores":
+            label = "large 256x%d, 8 waves" % op_large_width(w, torch.cuda.get_device_properties(0).multi_processor_count)
+        kernel = "gemm_op_kernel<%s> (%s)" % (method, label)
     mfma_dtype = "bf16" if meta["products"] == 3 else "f16"
     if t_mfma >= t_hbm:
         achieved = mfma_flops / (avg_launch_ms * 1e-3) / 1e12

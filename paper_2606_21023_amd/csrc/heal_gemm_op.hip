@@ -44,6 +44,8 @@
 #include "heal_device.h"
 #include "heal_internal.h"
 
+#include <atomic>
+
 namespace heal {
 
 namespace {
@@ -533,14 +535,61 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 #define HEAL_OP_WIDE_MIN_TILES 384
 #endif
 
+// The same with 224-column tiles (eight waves of 64 x 112), for shapes whose
+// 256-column tiles leave the last round of workgroups part-empty.
+#ifndef HEAL_OP_LARGE_FULL_N224_CFG
+#define HEAL_OP_LARGE_FULL_N224_CFG 256, 224, 64, 112, 512, 32
+#endif
+#ifndef HEAL_OP_LARGE_BASE_N224_CFG
+#define HEAL_OP_LARGE_BASE_N224_CFG 256, 224, 64, 112, 512, 64
+#endif
+#ifndef HEAL_OP_LARGE_PRESPLIT_N224_CFG
+#define HEAL_OP_LARGE_PRESPLIT_N224_CFG 256, 224, 64, 112, 512, 32
+#endif
+
+// Compute units of the current device, queried once per device.
+int device_cus()
+{
+    constexpr int kMaxDev = 64;
+    static std::atomic<int> cache[kMaxDev];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDev) return 256;
+    int n = cache[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+        n = 256;
+    cache[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
+// Relative time of a grid of 256 x bn tiles: the 256 x 256 instances hold
+// one workgroup per CU (LDS), so the grid runs in ceil(workgroups / CUs)
+// rounds, each as long as one tile, which grows with bn at fixed K.
+int64_t large_cost(const OpArgs &a, int bn, int cus)
+{
+    const int64_t wgs = ((a.M + 255) / 256) * ((a.N + bn - 1) / bn) * a.batch;
+    return (wgs + cus - 1) / cus * bn;
+}
+
 template <int OP>
 hipError_t launch_large(const OpArgs &a, hipStream_t stream)
 {
-    if constexpr (OP == OP_FULL) return launch_cfg<OP, HEAL_OP_LARGE_FULL_CFG>(a, stream);
-    else if constexpr (OP == OP_BASE) return launch_cfg<OP, HEAL_OP_LARGE_BASE_CFG>(a, stream);
-    else if constexpr (OP == OP_PRESPLIT)
-        return launch_cfg<OP, HEAL_OP_LARGE_PRESPLIT_CFG>(a, stream);
-    else return launch_cfg<OP, HEAL_OP_LARGE_CFG>(a, stream);
+    if constexpr (OP == OP_SCORES) {
+        return launch_cfg<OP, HEAL_OP_LARGE_CFG>(a, stream);
+    } else {
+        const int cus = device_cus();
+        const bool n224 = large_cost(a, 224, cus) < large_cost(a, 256, cus);
+        if constexpr (OP == OP_FULL)
+            return n224 ? launch_cfg<OP, HEAL_OP_LARGE_FULL_N224_CFG>(a, stream)
+                        : launch_cfg<OP, HEAL_OP_LARGE_FULL_CFG>(a, stream);
+        else if constexpr (OP == OP_BASE)
+            return n224 ? launch_cfg<OP, HEAL_OP_LARGE_BASE_N224_CFG>(a, stream)
+                        : launch_cfg<OP, HEAL_OP_LARGE_BASE_CFG>(a, stream);
+        else
+            return n224 ? launch_cfg<OP, HEAL_OP_LARGE_PRESPLIT_N224_CFG>(a, stream)
+                        : launch_cfg<OP, HEAL_OP_LARGE_PRESPLIT_CFG>(a, stream);
+    }
 }
 
 // HEAL-Full at M <= 64, wide N: eight waves of 64 x 32 (measured faster than

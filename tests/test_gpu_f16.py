@@ -248,6 +248,55 @@ def test_f16w_bitwise_invariants(products):
         assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "M=%d differs" % m
 
 
+def _large_widths_shapes():
+    """Two ragged shapes: one where the large instance keeps 256-column tiles
+    and one where 224-column tiles take fewer rounds of workgroups (one
+    workgroup per CU; the choice follows the device's CU count)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+
+    def cost(M, N, bn):
+        wgs = -(-M // 256) * -(-N // bn)
+        return -(-wgs // cus) * bn
+
+    tm = max(1, cus // 16)
+    wide = (256 * tm - 56, 256 * 16 - 6)                 # tm x 16 tiles: one round
+    narrow = (256 * 8 - 48, 224 * (-(-2 * cus // 8 // 8) * 8) - 36)
+    assert cost(*wide, 256) < cost(*wide, 224), wide
+    assert cost(*narrow, 224) < cost(*narrow, 256), narrow
+    return [wide, narrow]
+
+
+@pytest.mark.parametrize("K", [72, 37])
+def test_large_tile_widths(orc, K):
+    """Both tile widths of the large instance: the whole output bitwise equal
+    to the medium instance (and, pre-split, to heal_gemm_f32), sampled rows
+    against the oracle."""
+    for (M, N) in _large_widths_shapes():
+        A, W = f16w_case(M, N, K, seed=M + N + K)
+        e = heal.heal_f16_weight_exponent(float(np.abs(W).max()))
+        W16 = heal.heal_pack_f16_weight(to_dev(W), e)
+        Ad = to_dev(A)
+        rows = _rows(M, 6, K)
+        absprod = f16w_absprod(orc, A[rows], W, e)
+        for products in (1, 2):
+            announce("large widths f16w p%d %dx%dx%d" % (products, M, N, K))
+            C = heal.heal_gemm_f16w(Ad, W16, N, e, products, instance=heal.INSTANCE_LARGE)
+            Cm = heal.heal_gemm_f16w(Ad, W16, N, e, products, instance=heal.INSTANCE_MEDIUM)
+            torch.cuda.synchronize()
+            assert torch.equal(C.view(torch.int32), Cm.view(torch.int32)), "large != medium"
+            _, S = orc.gemm_f16w(A, W, e, products, rows=rows)
+            check_tolerance(C[torch.from_numpy(rows).cuda()].cpu().numpy(), S, absprod,
+                            "large widths p%d %dx%dx%d" % (products, M, N, K))
+            del C, Cm
+        announce("large widths presplit %dx%dx%d" % (M, N, K))
+        Bd = to_dev(np.ascontiguousarray(W.T))
+        Bp = heal.heal_presplit_b(Bd)
+        Cp = heal.heal_gemm_f32_presplit(Ad, Bp, N, instance=heal.INSTANCE_LARGE)
+        C0 = heal.heal_gemm_f32(Ad, Bd)
+        torch.cuda.synchronize()
+        assert torch.equal(Cp.view(torch.int32), C0.view(torch.int32)), "presplit differs"
+
+
 # ---------------------------------------------------------------------------
 # pre-split B: bitwise equal to heal_gemm_f32
 # ---------------------------------------------------------------------------
