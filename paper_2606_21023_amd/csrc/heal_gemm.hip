@@ -150,6 +150,7 @@ gemm_bf16x3_kernel(GemmArgs p)
     // Two LDS stage buffers as distinct objects, so the compiler can tell the
     // split's writes into one from the fragment reads of the other and
     // interleave them.
+    static_assert(2 * T::STAGE <= 160 * 1024, "two LDS stages must fit the 160 KB of a CU");
     __shared__ __attribute__((aligned(16))) char smem0[T::STAGE];
     __shared__ __attribute__((aligned(16))) char smem1[T::STAGE];
 

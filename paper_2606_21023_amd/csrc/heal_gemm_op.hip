@@ -133,6 +133,7 @@ gemm_op_kernel(OpArgs p)
     constexpr int B_IT = (B_UNITS + NT - 1) / NT;
     constexpr int ESZ_A = O::A_I16 ? 2 : 4;
 
+    static_assert(2 * STAGE <= 160 * 1024, "two LDS stages must fit the 160 KB of a CU");
     __shared__ __attribute__((aligned(16))) char smem0[STAGE];
     __shared__ __attribute__((aligned(16))) char smem1[STAGE];
 

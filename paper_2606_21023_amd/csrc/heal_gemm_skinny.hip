@@ -55,7 +55,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, i
 // 2*BK).  The LDS has 64 four-byte banks (256-byte bank lines).
 //  * chunk swizzle: the 16-byte chunk c of row r is stored at c ^ swz(r),
 //    so the 16 lanes of a fragment read (16 rows, one chunk) hit 16
-//    different 16-byte bank slots;
+//    different 16-byte bank slots; with rows of 256 bytes or more, odd
+//    16-row groups also flip bit 1, which keeps the row-contiguous B map
+//    of 32-column strips (below) free of store conflicts;
 //  * brow: the LDS row of B column n (B stored K x N), chosen so that one
 //    transposed 8-byte store instruction (32 lanes per cycle) covers all
 //    banks; it permutes rows within aligned groups of 16, which fragment
@@ -66,7 +68,8 @@ struct Lds {
     static_assert(BK == 32 || BK == 64 || BK >= 128, "stage depth");
     static __device__ __forceinline__ int swz(int row)
     {
-        return RP >= 256 ? (row & 15) : RP == 128 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+        return RP >= 256 ? ((row & 15) ^ ((row >> 3) & 2)) : RP == 128 ? ((row >> 1) & 7)
+                                                                         : ((row >> 2) & 3);
     }
     static __device__ __forceinline__ int brow(int n)
     {
@@ -112,6 +115,7 @@ gemm_skinny_kernel(GemmArgs p)
     constexpr int BM = 16 * MB, BN = 16 * CB, KQ = BK / 4, RP = L::RP;
     constexpr int A_PLANE = BM * RP, B_PLANE = BN * RP;
     constexpr int STAGE = 2 * A_PLANE + 2 * B_PLANE;
+    static_assert(2 * STAGE <= 160 * 1024, "two LDS stages must fit the 160 KB of a CU");
     // per thread and stage: NA quads of A; NB quads of B (N x K) or NB/4
     // 4x4 blocks of B (K x N)
     constexpr int NA = BM * KQ / kNT;
@@ -155,8 +159,15 @@ gemm_skinny_kernel(GemmArgs p)
         a_kq[u] = q % KQ;
         st_a[u] = L::quad_off(a_row[u], a_kq[u]);
     }
-    // B: N x K quads (like A), or K x N 4x4 blocks b = tid + 256u with
-    // k-quad b % KQ and column group b / KQ
+    // B: N x K quads (like A), or K x N 4x4 blocks b = tid + 256u.  Strips
+    // of 16 or 32 columns (64- or 128-byte row pieces) take the row map:
+    // column group b % (4 CB), k-quad b / (4 CB), so the lanes of one load
+    // instruction read whole row pieces (16 pieces per instruction rather
+    // than 64 quarter pieces: 1.4x faster on a 16 x 4096 x 4096 decode).
+    // Wider strips take column group b / KQ, k-quad b % KQ, which already
+    // reads whole 128-byte lines and has no store conflicts in their LDS
+    // geometry.
+    constexpr bool ROWMAP = CB <= 2 && RP >= 256;
     int b_kq[NB], b_n[NB], st_b[NB];
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
@@ -167,8 +178,13 @@ gemm_skinny_kernel(GemmArgs p)
             st_b[u] = L::quad_off(b_n[u], b_kq[u]);
         } else {
             const int bl = tid + kNT * (u >> 2), nn = u & 3;
-            b_kq[u] = bl % KQ;
-            b_n[u] = 4 * (bl / KQ) + nn;              // column of unit u
+            if (ROWMAP) {
+                b_kq[u] = bl / (4 * CB);
+                b_n[u] = 4 * (bl % (4 * CB)) + nn;
+            } else {
+                b_kq[u] = bl % KQ;
+                b_n[u] = 4 * (bl / KQ) + nn;          // column of unit u
+            }
             st_b[u] = L::quad_off(L::brow(b_n[u]), b_kq[u]);
         }
     }
@@ -378,22 +394,24 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 }
 
 // Strip width, stage depth and B ring depth by shape.  Measured on the
-// MI355X with a read-only kernel of the same access pattern (4096-deep B):
+// MI355X with read-only kernels of the same access pattern (4096-deep B):
 // 16-column strips read 64-byte pieces of rows that lie a full row pitch
-// apart and stream at ~2.7 TB/s, 32-column strips at ~5.5 TB/s, 128- and
-// 256-column strips at ~6.8 TB/s when there are enough of them.  Outputs
-// of 4096 columns have only 256 16-column strips, one per CU, which still
-// beats 128 wider ones; wide outputs (lm_head) use 256-column strips.  The
+// apart and stream at ~3.4-3.7 TB/s when each load instruction covers whole
+// pieces (~2.5 TB/s with quarter pieces), 32-column strips at ~5.5 TB/s,
+// 128- and 256-column strips at ~6.8 TB/s when there are enough of them.
+// Outputs of 4096 columns have only 256 16-column strips, one per CU, which
+// still beats 128 wider ones at every row count (32 rows: 27 vs 29 us; 64
+// rows: 38 vs 41 us); wide outputs (lm_head) use 256-column strips.  The
 // stage depth is the smallest that gives every thread whole 16-byte units
 // of A and B at the tile's row count.
 #ifndef HEAL_SKINNY_N1
 #define HEAL_SKINNY_N1 1, 256, 2      // M <= 16, narrow: CB, BK, R
 #endif
 #ifndef HEAL_SKINNY_N2
-#define HEAL_SKINNY_N2 2, 256, 2
+#define HEAL_SKINNY_N2 1, 256, 2
 #endif
 #ifndef HEAL_SKINNY_N4
-#define HEAL_SKINNY_N4 2, 128, 2
+#define HEAL_SKINNY_N4 1, 256, 2      // 160 KB of LDS: one workgroup per CU
 #endif
 #ifndef HEAL_SKINNY_W1
 #define HEAL_SKINNY_W1 8, 128, 2      // M <= 16, wide (strips of 16*CB columns)
