@@ -100,7 +100,11 @@ __device__ __forceinline__ u32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff)
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, 0));
 }
 
-template <int OP, int BM, int BN, int WM, int WN, int NT, int BK, bool VEC>
+// R: register sets of staged operands.  R = 1: the next stage is loaded
+// while the current one is multiplied out (one stage of compute to hide the
+// load).  R = 2: a ring of two sets, each reloaded two stages ahead, for
+// narrow tiles whose compute per stage is too short to hide a load.
+template <int OP, int BM, int BN, int WM, int WN, int NT, int BK, int R, bool VEC>
 __global__ void __launch_bounds__(NT)
 gemm_op_kernel(OpArgs p)
 {
@@ -119,6 +123,7 @@ gemm_op_kernel(OpArgs p)
     // and convert (extra waves only help move a narrow tile's operands)
     constexpr int CWAVES = WAVES_M * (BN / WN);
     static_assert(BK % 32 == 0 && BK <= 256, "stage depth");
+    static_assert(R == 1 || R == 2, "register sets");
     static_assert(BM % WM == 0 && BN % WN == 0 && WM % 16 == 0 && WN % 16 == 0, "wave tiling");
     static_assert(CWAVES * 64 <= NT && NT % 64 == 0, "compute waves exceed the workgroup");
 
@@ -190,10 +195,10 @@ gemm_op_kernel(OpArgs p)
 #pragma unroll
             for (int i = 0; i < FM; ++i) acc[j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-        u32x4 ra[A_IT], rb[B_IT];
+        u32x4 ra[R][A_IT], rb[R][B_IT];
 
-        // ---- global -> registers for the stage starting at k0 -------------
-        auto load_stage = [&](int64_t k0) {
+        // ---- global -> register set `set` for the stage starting at k0 ---
+        auto load_stage = [&](int set, int64_t k0) {
 #pragma unroll
             for (int it = 0; it < A_IT; ++it) {
                 const int u = it * NT + tid;
@@ -204,7 +209,7 @@ gemm_op_kernel(OpArgs p)
                 if (VEC) {
                     const uint32_t off =
                         ok ? (uint32_t)(((int64_t)row * p.lda + k) * ESZ_A) : kOOB;
-                    ra[it] = bload(rsrc_a, off);
+                    ra[set][it] = bload(rsrc_a, off);
                 } else {
                     u32x4 v = {0u, 0u, 0u, 0u};
                     if (m0 + row < M) {
@@ -224,7 +229,7 @@ gemm_op_kernel(OpArgs p)
                                 v[t] = k + t < K ? __builtin_bit_cast(uint32_t, f[t]) : 0u;
                         }
                     }
-                    ra[it] = v;
+                    ra[set][it] = v;
                 }
             }
 #pragma unroll
@@ -238,7 +243,7 @@ gemm_op_kernel(OpArgs p)
                         const bool ok = n0 + row < N && k < K;
                         const uint32_t off =
                             ok ? (uint32_t)(((int64_t)row * p.ldb + k) * 2) : kOOB;
-                        rb[it] = bload(rsrc_b, off);
+                        rb[set][it] = bload(rsrc_b, off);
                     } else {
                         u32x4 v = {0u, 0u, 0u, 0u};
                         if (n0 + row < N) {
@@ -251,7 +256,7 @@ gemm_op_kernel(OpArgs p)
                                 v[t / 2] = lo16 | (hi16 << 16);
                             }
                         }
-                        rb[it] = v;
+                        rb[set][it] = v;
                     }
                 } else {
                     // packed: block j of the tile, unit r = (ks * BP + plane) * 64 + lane
@@ -262,13 +267,13 @@ gemm_op_kernel(OpArgs p)
                         ok ? (uint32_t)(((int64_t)j * KC * O::BP * 64 + (k0 / 32) * O::BP * 64 + r) *
                                         16)
                            : kOOB;
-                    rb[it] = bload(rsrc_b, off);
+                    rb[set][it] = bload(rsrc_b, off);
                 }
             }
         };
 
-        // ---- registers -> LDS: convert A (and INT16 B), copy packed B -----
-        auto store_stage = [&](char *s) {
+        // ---- register set -> LDS: convert A (and INT16 B), copy packed B --
+        auto store_stage = [&](char *s, int set) {
             char *a0 = s, *a1 = s + A_PLANE;
             char *b0 = s + O::AP * A_PLANE, *b1 = b0 + B_PLANE;
 #pragma unroll
@@ -276,7 +281,7 @@ gemm_op_kernel(OpArgs p)
                 const int u = it * NT + tid;
                 if (A_UNITS % NT != 0 && u >= A_UNITS) continue;
                 const int row = u / A_UPR, c = u % A_UPR;
-                const u32x4 v = ra[it];
+                const u32x4 v = ra[set][it];
                 if constexpr (O::A_I16) {
                     u32x4 h, l;
 #pragma unroll
@@ -318,7 +323,7 @@ gemm_op_kernel(OpArgs p)
             for (int it = 0; it < B_IT; ++it) {
                 const int u = it * NT + tid;
                 if (B_UNITS % NT != 0 && u >= B_UNITS) continue;
-                const u32x4 v = rb[it];
+                const u32x4 v = rb[set][it];
                 if constexpr (O::B_ROWS) {
                     const int row = u / B_UPR, c = u % B_UPR;
                     u32x4 h, l;
@@ -398,20 +403,46 @@ gemm_op_kernel(OpArgs p)
         };
 
         // ---- main loop: two LDS stages, one barrier per stage -------------
-        auto step = [&](const char *cur, char *nxt, int64_t kt) {
-            if (kt + 1 < nk) load_stage((kt + 1) * BK);
-            if (computes) compute_stage(cur);
-            if (kt + 1 < nk) store_stage(nxt);
-            __syncthreads();
-        };
-        if (nk > 0) {
-            load_stage(0);
-            store_stage(smem0);
-            __syncthreads();
-        }
-        for (int64_t kt = 0; kt < nk; kt += 2) {
-            step(smem0, smem1, kt);
-            if (kt + 1 < nk) step(smem1, smem0, kt + 1);
+        if constexpr (R == 1) {
+            auto step = [&](const char *cur, char *nxt, int64_t kt) {
+                if (kt + 1 < nk) load_stage(0, (kt + 1) * BK);
+                if (computes) compute_stage(cur);
+                if (kt + 1 < nk) store_stage(nxt, 0);
+                __syncthreads();
+            };
+            if (nk > 0) {
+                load_stage(0, 0);
+                store_stage(smem0, 0);
+                __syncthreads();
+            }
+            for (int64_t kt = 0; kt < nk; kt += 2) {
+                step(smem0, smem1, kt);
+                if (kt + 1 < nk) step(smem1, smem0, kt + 1);
+            }
+        } else {
+            // stage t lives in register set t % 2; at step kt the set of
+            // stage kt+1 is stored and then reloaded with stage kt+3, so each
+            // load has two steps to arrive.  Reloads past the last stage are
+            // clamped to it (redundant loads whose data is never used).
+            const int64_t last = nk - 1;
+            auto clamp = [&](int64_t t) { return (t < last ? t : last) * BK; };
+            auto step = [&](const char *cur, char *nxt, int set, int64_t kt) {
+                if (computes) compute_stage(cur);
+                store_stage(nxt, set);
+                load_stage(set, clamp(kt + 3));
+                __syncthreads();
+            };
+            if (nk > 0) {
+                load_stage(0, 0);
+                store_stage(smem0, 0);
+                load_stage(1, clamp(1));
+                load_stage(0, clamp(2));
+                __syncthreads();
+            }
+            for (int64_t kt = 0; kt < nk; kt += 2) {
+                step(smem0, smem1, 1, kt);
+                if (kt + 1 < nk) step(smem1, smem0, 0, kt + 1);
+            }
         }
 
         // ---- epilogue: FP32 accumulators -> FP32 C, no downcast -----------
@@ -475,7 +506,7 @@ bool vec_path_applies(const OpArgs &a)
     return true;
 }
 
-template <int OP, int BM, int BN, int WM, int WN, int NT, int BK>
+template <int OP, int BM, int BN, int WM, int WN, int NT, int BK, int R = 1>
 hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 {
     const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
@@ -483,16 +514,16 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
     const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
     const dim3 grid((unsigned)tiles, gy);
     if (vec_path_applies<OP, BM, BN, BK>(a))
-        hipLaunchKernelGGL((gemm_op_kernel<OP, BM, BN, WM, WN, NT, BK, true>), grid, dim3(NT), 0,
-                           stream, a);
+        hipLaunchKernelGGL((gemm_op_kernel<OP, BM, BN, WM, WN, NT, BK, R, true>), grid, dim3(NT),
+                           0, stream, a);
     else
-        hipLaunchKernelGGL((gemm_op_kernel<OP, BM, BN, WM, WN, NT, BK, false>), grid, dim3(NT),
+        hipLaunchKernelGGL((gemm_op_kernel<OP, BM, BN, WM, WN, NT, BK, R, false>), grid, dim3(NT),
                            0, stream, a);
     return hipGetLastError();
 }
 
-// Instance configurations: BM, BN, WM, WN, threads, BK.  Threads beyond the
-// (BM/WM)(BN/WN) compute waves only load and convert.
+// Instance configurations: BM, BN, WM, WN, threads, BK[, register sets].
+// Threads beyond the (BM/WM)(BN/WN) compute waves only load and convert.
 #ifndef HEAL_OP_LARGE_CFG
 #define HEAL_OP_LARGE_CFG 128, 256, 64, 64, 512, 32
 #endif
@@ -521,15 +552,17 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 #define HEAL_OP_SKINNY64_CFG 64, 256, 64, 64, 256, 32
 #endif
 // M <= 64, narrow N (too few 256-column tiles to fill the chip): 16-column
-// tiles, one compute wave, three more waves that load and convert
+// tiles, one compute wave, three more waves that load and convert, and two
+// register sets (the stage's few MFMAs cannot hide a load: 1.1-1.4x faster
+// than one set on 16..64 x 4096 x 4096)
 #ifndef HEAL_OP_NARROW16_CFG
-#define HEAL_OP_NARROW16_CFG 16, 16, 16, 16, 256, 256
+#define HEAL_OP_NARROW16_CFG 16, 16, 16, 16, 256, 256, 2
 #endif
 #ifndef HEAL_OP_NARROW32_CFG
-#define HEAL_OP_NARROW32_CFG 32, 16, 32, 16, 256, 128
+#define HEAL_OP_NARROW32_CFG 32, 16, 32, 16, 256, 128, 2
 #endif
 #ifndef HEAL_OP_NARROW64_CFG
-#define HEAL_OP_NARROW64_CFG 64, 16, 64, 16, 256, 64
+#define HEAL_OP_NARROW64_CFG 64, 16, 64, 16, 256, 64, 2
 #endif
 // 256-column tiles are used while they number at least this many
 #ifndef HEAL_OP_WIDE_MIN_TILES
