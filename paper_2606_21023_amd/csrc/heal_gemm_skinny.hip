@@ -36,7 +36,6 @@ namespace heal {
 
 namespace {
 
-constexpr int kNT = 256;
 constexpr uint32_t kOOB = 0x80000000u;  // buffer offset beyond every range: reads 0
 
 __device__ __forceinline__ f32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff)
@@ -104,13 +103,15 @@ constexpr int skinny_occupancy(int MB, int CB, int BK)
 }
 
 // MB: 16-row blocks of the tile (M <= 16*MB); CB: 16-column blocks per
-// workgroup; BK: stage depth.
-// R: depth of the B register ring (stages in flight from HBM), even.
-template <int MB, int CB, int BK, int R, bool TRANS_B, bool ALPHA, bool TAIL>
-__global__ void __launch_bounds__(kNT, skinny_occupancy(MB, CB, BK))
+// workgroup; BK: stage depth; R: depth of the B register ring (stages in
+// flight from HBM), even; NT: threads (all load and split; the first
+// min(CB, 4) waves also multiply).
+template <int MB, int CB, int BK, int R, int NT, bool TRANS_B, bool ALPHA, bool TAIL>
+__global__ void __launch_bounds__(NT, skinny_occupancy(MB, CB, BK))
 gemm_skinny_kernel(GemmArgs p)
 {
     static_assert(R >= 2 && R % 2 == 0, "ring depth");
+    static_assert(BK <= 512, "stage depth (offset bounds of skinny_kernel_applies)");
     using L = Lds<BK>;
     constexpr int BM = 16 * MB, BN = 16 * CB, KQ = BK / 4, RP = L::RP;
     constexpr int A_PLANE = BM * RP, B_PLANE = BN * RP;
@@ -118,10 +119,11 @@ gemm_skinny_kernel(GemmArgs p)
     static_assert(2 * STAGE <= 160 * 1024, "two LDS stages must fit the 160 KB of a CU");
     // per thread and stage: NA quads of A; NB quads of B (N x K) or NB/4
     // 4x4 blocks of B (K x N)
-    constexpr int NA = BM * KQ / kNT;
-    constexpr int NB = BN * KQ / kNT;
-    static_assert(NA >= 1 && NA * kNT == BM * KQ, "A quads per thread");
-    static_assert(NB >= 1 && NB * kNT == BN * KQ, "B quads per thread");
+    constexpr int NA = BM * KQ / NT;
+    constexpr int NB = BN * KQ / NT;
+    static_assert(NT % 64 == 0 && NT <= 1024, "whole waves");
+    static_assert(NA >= 1 && NA * NT == BM * KQ, "A quads per thread");
+    static_assert(NB >= 1 && NB * NT == BN * KQ, "B quads per thread");
     static_assert(TRANS_B || NB % 4 == 0, "whole 4x4 B blocks per thread");
     constexpr int CW = CB < 4 ? CB : 4;         // waves that multiply
     constexpr int JW = CB / CW;                 // column blocks per computing wave
@@ -154,7 +156,7 @@ gemm_skinny_kernel(GemmArgs p)
     int a_row[NA], a_kq[NA], st_a[NA];
 #pragma unroll
     for (int u = 0; u < NA; ++u) {
-        const int q = tid + kNT * u;
+        const int q = tid + NT * u;
         a_row[u] = q / KQ;
         a_kq[u] = q % KQ;
         st_a[u] = L::quad_off(a_row[u], a_kq[u]);
@@ -172,12 +174,12 @@ gemm_skinny_kernel(GemmArgs p)
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
         if (TRANS_B) {
-            const int q = tid + kNT * u;
+            const int q = tid + NT * u;
             b_n[u] = q / KQ;
             b_kq[u] = q % KQ;
             st_b[u] = L::quad_off(b_n[u], b_kq[u]);
         } else {
-            const int bl = tid + kNT * (u >> 2), nn = u & 3;
+            const int bl = tid + NT * (u >> 2), nn = u & 3;
             if (ROWMAP) {
                 b_kq[u] = bl / (4 * CB);
                 b_n[u] = 4 * (bl % (4 * CB)) + nn;
@@ -369,28 +371,28 @@ gemm_skinny_kernel(GemmArgs p)
     }
 }
 
-template <int MB, int CB, int BK, int R, bool TRANS_B, bool ALPHA>
+template <int MB, int CB, int BK, int R, int NT, bool TRANS_B, bool ALPHA>
 hipError_t launch(const GemmArgs &a, hipStream_t stream)
 {
     const int64_t tiles = (a.N + 16 * CB - 1) / (16 * CB);
     const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
     if (a.K % BK)
-        hipLaunchKernelGGL((gemm_skinny_kernel<MB, CB, BK, R, TRANS_B, ALPHA, true>),
-                           dim3((unsigned)tiles, gy), dim3(kNT), 0, stream, a);
+        hipLaunchKernelGGL((gemm_skinny_kernel<MB, CB, BK, R, NT, TRANS_B, ALPHA, true>),
+                           dim3((unsigned)tiles, gy), dim3(NT), 0, stream, a);
     else
-        hipLaunchKernelGGL((gemm_skinny_kernel<MB, CB, BK, R, TRANS_B, ALPHA, false>),
-                           dim3((unsigned)tiles, gy), dim3(kNT), 0, stream, a);
+        hipLaunchKernelGGL((gemm_skinny_kernel<MB, CB, BK, R, NT, TRANS_B, ALPHA, false>),
+                           dim3((unsigned)tiles, gy), dim3(NT), 0, stream, a);
     return hipGetLastError();
 }
 
-template <int MB, int CB, int BK, int R>
+template <int MB, int CB, int BK, int R, int NT>
 hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
 {
     if (trans_b)
-        return use_alpha ? launch<MB, CB, BK, R, true, true>(a, stream)
-                         : launch<MB, CB, BK, R, true, false>(a, stream);
-    return use_alpha ? launch<MB, CB, BK, R, false, true>(a, stream)
-                     : launch<MB, CB, BK, R, false, false>(a, stream);
+        return use_alpha ? launch<MB, CB, BK, R, NT, true, true>(a, stream)
+                         : launch<MB, CB, BK, R, NT, true, false>(a, stream);
+    return use_alpha ? launch<MB, CB, BK, R, NT, false, true>(a, stream)
+                     : launch<MB, CB, BK, R, NT, false, false>(a, stream);
 }
 
 // Strip width, stage depth and B ring depth by shape.  Measured on the
@@ -405,22 +407,22 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 // stage depth is the smallest that gives every thread whole 16-byte units
 // of A and B at the tile's row count.
 #ifndef HEAL_SKINNY_N1
-#define HEAL_SKINNY_N1 1, 256, 2      // M <= 16, narrow: CB, BK, R
+#define HEAL_SKINNY_N1 1, 256, 2, 256      // M <= 16, narrow: CB, BK, R, NT
 #endif
 #ifndef HEAL_SKINNY_N2
-#define HEAL_SKINNY_N2 1, 256, 2
+#define HEAL_SKINNY_N2 1, 256, 2, 256
 #endif
 #ifndef HEAL_SKINNY_N4
-#define HEAL_SKINNY_N4 1, 256, 2      // 160 KB of LDS: one workgroup per CU
+#define HEAL_SKINNY_N4 1, 256, 2, 256      // 160 KB of LDS: one workgroup per CU
 #endif
 #ifndef HEAL_SKINNY_W1
-#define HEAL_SKINNY_W1 8, 128, 2      // M <= 16, wide (strips of 16*CB columns)
+#define HEAL_SKINNY_W1 8, 128, 2, 256      // M <= 16, wide (strips of 16*CB columns)
 #endif
 #ifndef HEAL_SKINNY_W2
-#define HEAL_SKINNY_W2 8, 64, 2
+#define HEAL_SKINNY_W2 8, 64, 2, 256
 #endif
 #ifndef HEAL_SKINNY_W4
-#define HEAL_SKINNY_W4 16, 32, 2
+#define HEAL_SKINNY_W4 16, 32, 2, 256
 #endif
 #ifndef HEAL_SKINNY_WIDE_MIN_N
 #define HEAL_SKINNY_WIDE_MIN_N 16384
@@ -447,13 +449,13 @@ bool skinny_kernel_applies(const GemmArgs &a, bool trans_b)
 {
     // At most 64 rows, 16-byte rows, whole quads along K (and N).  Buffer
     // offsets are 32-bit: the largest is that of the last element a lane may
-    // address, (M-1)*lda + K (+ one 256-deep stage for a clamped reload) for
-    // A, the same with the 256-row strip for B stored N x K, and
+    // address, (M-1)*lda + K (+ one stage, at most 512 deep, for a clamped
+    // reload) for A, the same with the 256-row strip for B stored N x K, and
     // (K+3)*ldb + 256 for B stored K x N (row k + kk of a 4-row block).
     if (a.M > 64 || !(a.vecA && a.vecB && a.vecC) || a.K % 4 != 0 || a.N % 4 != 0) return false;
     const int64_t lim = 0x7fffffffLL;
-    if (((a.M - 1) * a.lda + a.K + 256) * 4 >= lim) return false;
-    if (trans_b ? ((int64_t)255 * a.ldb + a.K + 256) * 4 >= lim : ((a.K + 3) * a.ldb + 256) * 4 >= lim)
+    if (((a.M - 1) * a.lda + a.K + 512) * 4 >= lim) return false;
+    if (trans_b ? ((int64_t)255 * a.ldb + a.K + 512) * 4 >= lim : ((a.K + 3) * a.ldb + 256) * 4 >= lim)
         return false;
     return (a.N + 15) / 16 <= 0x7fffffffLL;
 }
