@@ -34,10 +34,12 @@ Prints ONE JSON line:
   f16_base    heal_gemm_f16w, HEAL-Base: one FP16 product per chunk;
   i16_scores  heal_scores_i16 on the attention workload: Q and K quantized to
               INT16 before the timed region (as stored in the KV cache), four
-              FP16 products per chunk.
-For every method a step is one launch of its GEMM kernel over the workload;
-value is FP32-equivalent TFLOP/s (2*M*N*K*batch per step); the roofline uses
-the method's own MFMA flops and operand bytes.
+              FP16 products per chunk;
+  split       heal_split_f32 over the workload's B operand: value is GB/s
+              (8 bytes per element), HBM-bound.
+For every GEMM method a step is one launch of its GEMM kernel over the
+workload; value is FP32-equivalent TFLOP/s (2*M*N*K*batch per step); the
+roofline uses the method's own MFMA flops and operand bytes.
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--method NAME] [--no-cpu]
 """
@@ -65,7 +67,8 @@ KERNEL_NAMES = {1: "gemm_large8_kernel (256x256 tiles, 8 waves of 64x128)",
 KERNEL_SOURCES = {1: ["heal_gemm_large.hip", "heal_device.h", "heal_internal.h"],
                   2: ["heal_gemm.hip", "heal_device.h", "heal_internal.h"],
                   3: ["heal_gemm_skinny.hip", "heal_device.h", "heal_internal.h"],
-                  "op": ["heal_gemm_op.hip", "heal_device.h", "heal_internal.h"]}
+                  "op": ["heal_gemm_op.hip", "heal_device.h", "heal_internal.h"],
+                  "split": ["heal_split.hip", "heal_device.h", "heal_internal.h"]}
 OP_INSTANCE_NAMES = {1: "large 128x256, 8 waves", 2: "medium 128x128, 8 waves",
                      3: "skinny M<=64, 256-column tiles"}
 # MFMA products per 32-deep chunk and output block, and bytes per operand element
@@ -75,6 +78,7 @@ METHODS = {
     "f16_full": {"products": 2, "a_bytes": 4, "b_bytes": 2, "dtype": "f16x2-f32acc"},
     "f16_base": {"products": 1, "a_bytes": 4, "b_bytes": 2, "dtype": "f16-f32acc"},
     "i16_scores": {"products": 4, "a_bytes": 2, "b_bytes": 2, "dtype": "i16-dual-f16-f32acc"},
+    "split": {"products": 0, "a_bytes": 0, "b_bytes": 4, "dtype": "f32->bf16x2"},
 }
 
 
@@ -163,6 +167,107 @@ def cpu_baseline(w, A, B, target_s, method="bf16x3", extra=None):
                                                 w.batch, what)}
 
 
+def bench_split(args, w):
+    """heal_split_f32 over the workload's B operand (K x N FP32 elements):
+    4 bytes read and 2 + 2 bytes written per element, HBM-bound."""
+    import ctypes
+    import torch
+    import paper_2606_21023_amd as heal
+    from paper_2606_21023_amd import workloads as wl
+
+    _, B = wl.make_inputs(w)
+    X = np.ascontiguousarray(B[0] if B.ndim == 3 else B).reshape(-1)
+    n = X.size
+    alg_bytes = 8.0 * n
+    dev = torch.device("cuda:0")
+    n_rot = int(min(16, max(1, math.ceil(float(1 << 30) / alg_bytes))))
+    sets = []
+    for _ in range(n_rot):
+        xd = torch.from_numpy(X).to(dev)
+        sets.append((xd, torch.empty(n, dtype=torch.uint16, device=dev),
+                     torch.empty(n, dtype=torch.uint16, device=dev)))
+    torch.cuda.synchronize()
+    L = heal.lib()
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    calls = [(s[0].data_ptr(), s[1].data_ptr(), s[2].data_ptr(), n, sp) for s in sets]
+
+    def run(i):
+        st = L.heal_split_f32(*calls[i % n_rot])
+        if st != 0:
+            raise heal.HealError("launch failed with status %d" % st)
+
+    for i in range(args.warmup):
+        run(i)
+    run(0)
+    torch.cuda.synchronize()
+    first = (sets[0][1].clone(), sets[0][2].clone())
+    e_start = torch.cuda.Event(enable_timing=True)
+    e_end = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e_start.record(stream)
+    for i in range(args.steps):
+        run(i)
+    e_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    identical = all(torch.equal(s[1], first[0]) and torch.equal(s[2], first[1])
+                    for s in sets[:min(n_rot, args.steps)])
+    ms = e_start.elapsed_time(e_end) / args.steps
+    gbs = alg_bytes / (ms * 1e-3) / 1e9
+    traffic = measured_traffic("split:%s" % w.name, "split")
+    roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4),
+                "traffic": None if traffic is None else round(traffic),
+                "kernel": "split_kernel<true> (8 elements per thread and step)",
+                "per_launch": "8*n bytes (4 read, 2+2 written per element) = %.4g" % alg_bytes,
+                "avg_launch_us": round(ms * 1e3, 2)}
+    cpu = None
+    if not args.no_cpu:
+        from oracle import oracle
+        orc = oracle.default()
+        m = min(n, 1 << 20)
+        while True:
+            t1 = time.perf_counter()
+            orc.split(X[:m])
+            t = time.perf_counter() - t1
+            if t >= args.cpu_seconds or m >= n:
+                break
+            m = min(n, m * max(2, int(args.cpu_seconds / max(t, 1e-3))))
+        cpu = {"value": round(8.0 * m / t / 1e9, 3), "unit": "GB/s", "cores": orc.num_threads(),
+               "kind": "oracle", "seconds": round(t, 3),
+               "sample": "split oracle: first %d of the %d elements of the %s B operand"
+                         % (m, n, w.name)}
+    line = {
+        "metric": "GB/s of heal_split_f32 (FP32 -> bf16 hi, lo planes); % of HBM peak; bit-repro",
+        "value": round(gbs, 1),
+        "unit": "GB/s (8 bytes per element)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": METHODS["split"]["dtype"],
+        "data": "synthetic",
+        "config": {"workload": w.name, "method": "split", "elements": n,
+                   "inputs": "the B operand of: " + w.note, "operand_copies_rotated": n_rot},
+        "bit_repro": {"runs": args.steps + args.warmup + 1, "identical": identical},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "wall_s": round(wall, 3),
+    }
+    print(json.dumps(line))
+    sys.stdout.flush()
+    if args.copy_calibration:
+        src = torch.ones(256 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -177,6 +282,8 @@ def main():
 
     method = args.method
     w = wl.WORKLOADS[args.workload]
+    if method == "split":
+        return bench_split(args, w)
     if method == "i16_scores" and w.name != "attn_scores":
         print("--method i16_scores runs on the attn_scores workload", file=sys.stderr)
         sys.exit(2)
