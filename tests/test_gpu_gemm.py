@@ -261,6 +261,25 @@ def test_instances_bitwise_equal(shape):
             "%s differs from large" % INAME[inst]
 
 
+@pytest.mark.parametrize("N,K", [(1040, 1028), (300, 520), (16400, 260)],
+                         ids=["narrow-ktail", "narrow-ragged-n", "wide"])
+def test_skinny_every_m_bitwise(N, K):
+    """Every row count 1..64 through the skinny instance (16-row, 32-row and
+    64-row tiles; narrow strips with the row-contiguous B map, and wide
+    strips), B stored K x N with a K tail and a ragged last strip: each row
+    bitwise equal to the medium instance's row of the full 64-row product."""
+    A = wl.random_matrix((64, K), seed=N + K)
+    B = wl.random_matrix((K, N), seed=N + 2 * K)
+    Ad, Bd = to_dev(A), to_dev(B)
+    announce("skinny every M %dx%d" % (N, K))
+    ref = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Bd)
+    torch.cuda.synchronize()
+    for m in range(1, 65):
+        C = heal.heal_gemm_f32_instance(heal.INSTANCE_SKINNY, Ad[:m], Bd)
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "M=%d differs" % m
+
+
 def test_entry_points_bitwise_equal():
     M, N, K = 200, 300, 333
     A = wl.random_matrix((M, K), seed=31)
