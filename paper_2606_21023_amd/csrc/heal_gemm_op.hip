@@ -528,9 +528,11 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 #define HEAL_OP_LARGE_CFG 128, 256, 64, 64, 512, 32
 #endif
 // 256 x 256 tiles, eight waves of 64 x 128 (128 accumulator VGPRs at two
-// waves per SIMD)
+// waves per SIMD).  HEAL-Full keeps two register sets (1.03x faster at
+// 8192^3, 1.06x at 2048 x 14336 x 4096, despite 8 spilled VGPRs); Base and
+// the pre-split product were no faster or slower with two.
 #ifndef HEAL_OP_LARGE_FULL_CFG
-#define HEAL_OP_LARGE_FULL_CFG 256, 256, 64, 128, 512, 32
+#define HEAL_OP_LARGE_FULL_CFG 256, 256, 64, 128, 512, 32, 2
 #endif
 #ifndef HEAL_OP_LARGE_BASE_CFG
 #define HEAL_OP_LARGE_BASE_CFG 256, 256, 64, 128, 512, 64
@@ -572,7 +574,7 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 // The same with 224-column tiles (eight waves of 64 x 112), for shapes whose
 // 256-column tiles leave the last round of workgroups part-empty.
 #ifndef HEAL_OP_LARGE_FULL_N224_CFG
-#define HEAL_OP_LARGE_FULL_N224_CFG 256, 224, 64, 112, 512, 32
+#define HEAL_OP_LARGE_FULL_N224_CFG 256, 224, 64, 112, 512, 32, 2
 #endif
 #ifndef HEAL_OP_LARGE_BASE_N224_CFG
 #define HEAL_OP_LARGE_BASE_N224_CFG 256, 224, 64, 112, 512, 64
