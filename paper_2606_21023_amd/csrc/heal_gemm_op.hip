@@ -554,17 +554,19 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 #define HEAL_OP_SKINNY64_CFG 64, 256, 64, 64, 256, 32
 #endif
 // M <= 64, narrow N (too few 256-column tiles to fill the chip): 16-column
-// tiles, one compute wave, three more waves that load and convert, and two
-// register sets (the stage's few MFMAs cannot hide a load: 1.1-1.4x faster
-// than one set on 16..64 x 4096 x 4096)
+// tiles, one compute wave and 7 or 15 more waves that load and convert, and
+// two register sets (the stage's few MFMAs cannot hide a load: 1.1-1.4x
+// faster than one set on 16..64 x 4096 x 4096).  Measured on those shapes,
+// 512 threads beat 256 by 1.09-1.13x at 16 and 32 rows (HEAL-Full and the
+// pre-split product), 1024 threads beat 256 by 1.09-1.15x at 64 rows.
 #ifndef HEAL_OP_NARROW16_CFG
-#define HEAL_OP_NARROW16_CFG 16, 16, 16, 16, 256, 256, 2
+#define HEAL_OP_NARROW16_CFG 16, 16, 16, 16, 512, 256, 2
 #endif
 #ifndef HEAL_OP_NARROW32_CFG
-#define HEAL_OP_NARROW32_CFG 32, 16, 32, 16, 256, 128, 2
+#define HEAL_OP_NARROW32_CFG 32, 16, 32, 16, 512, 128, 2
 #endif
 #ifndef HEAL_OP_NARROW64_CFG
-#define HEAL_OP_NARROW64_CFG 64, 16, 64, 16, 256, 64, 2
+#define HEAL_OP_NARROW64_CFG 64, 16, 64, 16, 1024, 64, 2
 #endif
 // 256-column tiles are used while they number at least this many
 #ifndef HEAL_OP_WIDE_MIN_TILES
