@@ -124,7 +124,7 @@ gemm_skinny_kernel(GemmArgs p)
     static_assert(NT % 64 == 0 && NT <= 1024, "whole waves");
     static_assert(NA >= 1 && NA * NT == BM * KQ, "A quads per thread");
     static_assert(NB >= 1 && NB * NT == BN * KQ, "B quads per thread");
-    static_assert(TRANS_B || NB % 4 == 0, "whole 4x4 B blocks per thread");
+    static_assert(TRANS_B || NB % 4 == 0 || NB == 2, "whole or half 4x4 B blocks per thread");
     constexpr int CW = CB < 4 ? CB : 4;         // waves that multiply
     constexpr int JW = CB / CW;                 // column blocks per computing wave
     static_assert(CB % CW == 0, "column blocks per wave");
@@ -169,8 +169,16 @@ gemm_skinny_kernel(GemmArgs p)
     // Wider strips take column group b / KQ, k-quad b % KQ, which already
     // reads whole 128-byte lines and has no store conflicts in their LDS
     // geometry.
+    // With two units per thread (HALF: twice as many threads as 4x4
+    // blocks), a thread loads two rows of a block: column group t % (4 CB),
+    // row pair (t / (4 CB)) % 2, k-quad t / (8 CB); one load instruction
+    // still reads 16 whole row pieces, and its transposed 4-byte stores
+    // (k pairs) fill all 64 banks.
     constexpr bool ROWMAP = CB <= 2 && RP >= 256;
-    int b_kq[NB], b_n[NB], st_b[NB];
+    constexpr bool HALF = !TRANS_B && NB == 2;
+    static_assert(!HALF || ROWMAP, "half blocks use the row map");
+    int b_kq[NB], b_n[NB], st_b[NB], b_r0[NB];
+    int st_h[4] = {0, 0, 0, 0};                  // HALF: LDS offset of column 4c + nn
 #pragma unroll
     for (int u = 0; u < NB; ++u) {
         if (TRANS_B) {
@@ -178,6 +186,16 @@ gemm_skinny_kernel(GemmArgs p)
             b_n[u] = q / KQ;
             b_kq[u] = q % KQ;
             st_b[u] = L::quad_off(b_n[u], b_kq[u]);
+            b_r0[u] = 0;
+        } else if (HALF) {
+            const int c = tid % (4 * CB), half = (tid / (4 * CB)) & 1;
+            b_kq[u] = tid / (8 * CB);
+            b_n[u] = 4 * c;
+            b_r0[u] = 4 * b_kq[u] + 2 * half;    // first of the thread's two rows
+            st_b[u] = 0;
+#pragma unroll
+            for (int nn = 0; nn < 4; ++nn)
+                st_h[nn] = L::quad_off(L::brow(4 * c + nn), b_kq[u]) + 4 * half;
         } else {
             const int bl = tid + NT * (u >> 2), nn = u & 3;
             if (ROWMAP) {
@@ -188,6 +206,7 @@ gemm_skinny_kernel(GemmArgs p)
                 b_n[u] = 4 * (bl / KQ) + nn;          // column of unit u
             }
             st_b[u] = L::quad_off(L::brow(b_n[u]), b_kq[u]);
+            b_r0[u] = 4 * b_kq[u];
         }
     }
     const int wj0 = wave;                        // first column block of this wave
@@ -211,7 +230,7 @@ gemm_skinny_kernel(GemmArgs p)
                 vb[u] = b_n[u] < cols ? (uint32_t)((b_n[u] * p.ldb + 4 * b_kq[u]) * 4) : kOOB;
             else {
                 const int nq4 = b_n[u] & ~3;         // first column of the block
-                vb[u] = nq4 < cols ? (uint32_t)((4 * b_kq[u] * p.ldb + nq4) * 4) : kOOB;
+                vb[u] = nq4 < cols ? (uint32_t)((b_r0[u] * p.ldb + nq4) * 4) : kOOB;
             }
         }
         const int ldb4 = (int)(p.ldb * 4);
@@ -235,9 +254,9 @@ gemm_skinny_kernel(GemmArgs p)
                     if (TAIL && s * BK + 4 * b_kq[u] >= k_end) v = kOOB;
                     xb[set][u] = bload(rb_src, v, s * BK * 4);
                 } else {
-                    // row kk = u & 3 of block u >> 2
-                    const int kk = u & 3;
-                    if (TAIL && s * BK + 4 * b_kq[u] + kk >= k_end) v = kOOB;
+                    // row kk = u & 3 of block u >> 2 (HALF: row u of the pair)
+                    const int kk = HALF ? u : (u & 3);
+                    if (TAIL && s * BK + b_r0[u] + kk >= k_end) v = kOOB;
                     xb[set][u] = bload(rb_src, v, (s * BK + kk) * ldb4);
                 }
             }
@@ -254,20 +273,31 @@ gemm_skinny_kernel(GemmArgs p)
         };
         auto split_b = [&](char *st, int set) {
             char *bh = st + 2 * A_PLANE, *bl = bh + B_PLANE;
+            if constexpr (HALF) {
+                // column nn of the block: element nn of the thread's two rows
 #pragma unroll
-            for (int u = 0; u < NB; ++u) {
-                uint32_t h0, l0, h1, l1;
-                if (TRANS_B) {
-                    split2(xb[set][u].x, xb[set][u].y, h0, l0);
-                    split2(xb[set][u].z, xb[set][u].w, h1, l1);
-                } else {
-                    // column nn of the block: element nn of its four rows
-                    const int blk = u >> 2, nn = u & 3;
-                    split2(xb[set][4 * blk + 0][nn], xb[set][4 * blk + 1][nn], h0, l0);
-                    split2(xb[set][4 * blk + 2][nn], xb[set][4 * blk + 3][nn], h1, l1);
+                for (int nn = 0; nn < 4; ++nn) {
+                    uint32_t h, l;
+                    split2(xb[set][0][nn], xb[set][1][nn], h, l);
+                    *reinterpret_cast<uint32_t *>(bh + st_h[nn]) = h;
+                    *reinterpret_cast<uint32_t *>(bl + st_h[nn]) = l;
                 }
-                lds_store2(bh, st_b[u], h0, h1);
-                lds_store2(bl, st_b[u], l0, l1);
+            } else {
+#pragma unroll
+                for (int u = 0; u < NB; ++u) {
+                    uint32_t h0, l0, h1, l1;
+                    if (TRANS_B) {
+                        split2(xb[set][u].x, xb[set][u].y, h0, l0);
+                        split2(xb[set][u].z, xb[set][u].w, h1, l1);
+                    } else {
+                        // column nn of the block: element nn of its four rows
+                        const int blk = u >> 2, nn = u & 3;
+                        split2(xb[set][4 * blk + 0][nn], xb[set][4 * blk + 1][nn], h0, l0);
+                        split2(xb[set][4 * blk + 2][nn], xb[set][4 * blk + 3][nn], h1, l1);
+                    }
+                    lds_store2(bh, st_b[u], h0, h1);
+                    lds_store2(bl, st_b[u], l0, l1);
+                }
             }
         };
 
@@ -405,15 +435,17 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 // still beats 128 wider ones at every row count (32 rows: 27 vs 29 us; 64
 // rows: 38 vs 41 us); wide outputs (lm_head) use 256-column strips.  The
 // stage depth is the smallest that gives every thread whole 16-byte units
-// of A and B at the tile's row count.
+// of A and B at the tile's row count.  Narrow strips run 512 threads (half
+// blocks of B): 64 rows 33.6 vs 37.6 us with 256, 1 to 32 rows the same or
+// slightly faster.
 #ifndef HEAL_SKINNY_N1
-#define HEAL_SKINNY_N1 1, 256, 2, 256      // M <= 16, narrow: CB, BK, R, NT
+#define HEAL_SKINNY_N1 1, 256, 2, 512      // M <= 16, narrow: CB, BK, R, NT
 #endif
 #ifndef HEAL_SKINNY_N2
-#define HEAL_SKINNY_N2 1, 256, 2, 256
+#define HEAL_SKINNY_N2 1, 256, 2, 512
 #endif
 #ifndef HEAL_SKINNY_N4
-#define HEAL_SKINNY_N4 1, 256, 2, 256      // 160 KB of LDS: one workgroup per CU
+#define HEAL_SKINNY_N4 1, 256, 2, 512      // 160 KB of LDS: one workgroup per CU
 #endif
 #ifndef HEAL_SKINNY_W1
 #define HEAL_SKINNY_W1 8, 128, 2, 256      // M <= 16, wide (strips of 16*CB columns)
