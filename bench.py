@@ -25,6 +25,9 @@ Prints ONE JSON line:
   cpu_baseline the CPU oracle timed on a bounded row sample of the same product
   comparison   MI355X native FP32 GEMM (torch.matmul, TF32 off) on the same inputs
   bit_repro    every timed step's output bitwise equal to the first
+  step_stats   median, minimum and standard error of the per-launch times
+               of a second pass of the same launches with an event between
+               each (the paper's timing convention), after the timed region
 
 --method selects the product (default bf16x3, the line above):
   presplit    heal_gemm_f32_presplit: B split once into packed bf16 (hi, lo)
@@ -167,6 +170,24 @@ def cpu_baseline(w, A, B, target_s, method="bf16x3", extra=None):
                                                 w.batch, what)}
 
 
+def step_stats(run, steps, stream):
+    """Per-launch durations from one HIP event before and after every launch,
+    in a pass of its own after the timed region (so that the timed region
+    holds nothing but the launches): median, minimum and standard error of
+    the mean, in ms."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record(stream)
+    for i in range(steps):
+        run(i)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    d = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)], dtype=np.float64)
+    sem = float(d.std(ddof=1) / math.sqrt(len(d))) if len(d) > 1 else 0.0
+    return {"launches": steps, "median_ms": round(float(np.median(d)), 5),
+            "min_ms": round(float(d.min()), 5), "sem_ms": round(sem, 6)}
+
+
 def bench_split(args, w):
     """heal_split_f32 over the workload's B operand (K x N FP32 elements):
     4 bytes read and 2 + 2 bytes written per element, HBM-bound."""
@@ -214,6 +235,7 @@ def bench_split(args, w):
     identical = all(torch.equal(s[1], first[0]) and torch.equal(s[2], first[1])
                     for s in sets[:min(n_rot, args.steps)])
     ms = e_start.elapsed_time(e_end) / args.steps
+    stats = step_stats(run, args.steps, stream)
     gbs = alg_bytes / (ms * 1e-3) / 1e9
     traffic = measured_traffic("split:%s" % w.name, "split")
     roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -254,6 +276,7 @@ def bench_split(args, w):
         "config": {"workload": w.name, "method": "split", "elements": n,
                    "inputs": "the B operand of: " + w.note, "operand_copies_rotated": n_rot},
         "bit_repro": {"runs": args.steps + args.warmup + 1, "identical": identical},
+        "step_stats": stats,
         "roofline": roofline,
         "cpu_baseline": cpu,
         "wall_s": round(wall, 3),
@@ -396,6 +419,7 @@ def main():
     identical = all(bool(torch.equal(s[2].view(torch.int32), first.view(torch.int32)))
                     for s in sets[:min(n_rot, args.steps)])
     total_ms = e_start.elapsed_time(e_end)
+    stats = step_stats(run, args.steps, stream)
     ms_per_step = total_ms / args.steps
     # launches run back to back on one stream: the mean launch duration is
     # the timed region over the number of launches
@@ -487,6 +511,7 @@ def main():
         "pct_of_bf16_peak_div3": round(100.0 * value / (BF16_DENSE_PEAK_TFLOPS / 3), 2),
         "hbm_gbs": round(alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "bit_repro": {"runs": args.steps + args.warmup + 1, "identical": identical},
+        "step_stats": stats,
         "roofline": roofline,
         "cpu_baseline": cpu,
         "comparison": comparison,
