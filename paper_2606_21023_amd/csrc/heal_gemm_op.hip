@@ -472,7 +472,9 @@ gemm_op_kernel(OpArgs p)
                 if (m < M && n < N) {
                     float *cp = C + m * p.ldc + n;
                     if (p.vecC && n + 4 <= N) {
-                        *reinterpret_cast<f32x4 *>(cp) = v;
+                        // streaming store: C is not read again here (INT16
+                        // scores 1.07x, lm_head 1.01-1.035x, others unchanged)
+                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(cp));
                     } else {
                         cp[0] = v.x;
                         if (n + 1 < N) cp[1] = v.y;
