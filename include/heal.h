@@ -124,7 +124,10 @@ heal_status_t heal_gemm_f32_strided_batched(int64_t M, int64_t N, int64_t K, flo
  */
 typedef enum heal_instance_t {
     HEAL_INSTANCE_AUTO = 0,
-    HEAL_INSTANCE_LARGE = 1,   /* 256 x 256 output tiles, compute-bound shapes */
+    HEAL_INSTANCE_LARGE = 1,   /* 256 x 256 output tiles (the FP16 and pre-split
+                                  products take 256 x 224 where that needs fewer
+                                  rounds of workgroups; INT16 scores 128 x 256),
+                                  compute-bound shapes */
     HEAL_INSTANCE_MEDIUM = 2,  /* 128 x 128 output tiles */
     HEAL_INSTANCE_SKINNY = 3,  /* M <= 64: decode and lm_head shapes, B streamed */
     HEAL_INSTANCE_COUNT = 4
