@@ -103,15 +103,6 @@ def parse():
     return ap.parse_args()
 
 
-def op_large_width(w, cus):
-    """Tile width the large FP16 / pre-split instance picks for workload w:
-    224 columns when that takes fewer rounds of one workgroup per CU."""
-    def cost(bn):
-        wgs = -(-w.M // 256) * -(-w.N // bn) * w.batch
-        return -(-wgs // cus) * bn
-    return 224 if cost(224) < cost(256) else 256
-
-
 def kernel_source_hash(instance):
     """Hash of the sources of the kernel an instance launches ("op": heal_gemm_op.hip)."""
     h = hashlib.sha256()
@@ -437,9 +428,11 @@ def main():
     else:
         traffic = measured_traffic("%s:%s" % (method, w.name), "op")
         label = OP_INSTANCE_NAMES.get(instance, "?")
+        kname = "gemm_op_kernel"
         if instance == 1 and method != "i16_scores":
-            label = "large 256x%d, 8 waves" % op_large_width(w, torch.cuda.get_device_properties(0).multi_processor_count)
-        kernel = "gemm_op_kernel<%s> (%s)" % (method, label)
+            # 16-byte aligned rows: the hand-scheduled 256 x 256 kernel
+            kname, label = "gemm_op8_kernel", "large 256x256, 8 waves of 64x128, hand-scheduled"
+        kernel = "%s<%s> (%s)" % (kname, method, label)
     mfma_dtype = "bf16" if meta["products"] == 3 else "f16"
     if t_mfma >= t_hbm:
         achieved = mfma_flops / (avg_launch_ms * 1e-3) / 1e12

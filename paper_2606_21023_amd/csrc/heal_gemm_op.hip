@@ -488,6 +488,279 @@ gemm_op_kernel(OpArgs p)
     }
 }
 
+// The packed-weight products at 256 x 256 tiles with the schedule of the
+// large bf16x3 kernel: eight waves of 64 x 128, one 32-deep stage per barrier,
+// two LDS stages.  While stage s is multiplied out, each staged register group
+// of stage s+1 is converted into the other LDS buffer between the MFMAs of one
+// column block and at once reloaded with stage s+2.  Per stage and thread:
+// four 16-byte quads of A (rows tid/8 + 64u, k-quad tid%8), converted in the
+// generic kernel's LDS layout (HEAL-Full: the FP16 pair; HEAL-Base: one FP16
+// plane; pre-split: the bf16 pair), and 2 BP 16-byte units of the packed B
+// (units tid + 512v of the tile's 16 column blocks), copied to LDS in fragment
+// order.  Same products in the same order as the generic kernel, so the bits
+// are the same.
+#ifndef HEAL_OP_LARGE8
+#define HEAL_OP_LARGE8 1
+#endif
+#ifndef HEAL_OP_N224
+#define HEAL_OP_N224 1
+#endif
+
+template <int OP, bool TAIL>
+__global__ void __launch_bounds__(512, 1)
+gemm_op8_kernel(OpArgs p)
+{
+    using O = OpT<OP>;
+    static_assert(!O::A_I16 && !O::B_ROWS, "packed-weight products only");
+    constexpr bool BF16 = OP == OP_PRESPLIT;
+    constexpr int NT = 512, BM = 256, BN = 256, BK = 32, ROWB = 2 * BK;
+    constexpr int A_PLANE = BM * ROWB;           // 16 KB per 16-bit plane of A
+    constexpr int B_BYTES = (BN / 16) * O::BP * 1024;  // 16 column blocks, fragment order
+    constexpr int STAGE = O::AP * A_PLANE + B_BYTES;
+    constexpr int NBU = 2 * O::BP;               // B units per thread and stage
+    constexpr int NU = 4 + NBU;                  // conversion units per thread and stage
+    constexpr int MF = 4 * (OP == OP_BASE ? 1 : OP == OP_FULL ? 2 : 3);  // MFMAs per column block
+    static_assert(NU <= 8, "one unit per column block");
+    static_assert(2 * STAGE <= 160 * 1024, "two LDS stages must fit the 160 KB of a CU");
+    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave & 3, wn = wave >> 2;
+    const int fr = lane & 15, fg = lane >> 4;
+    auto swz = [](int row) { return (row >> 1) & 3; };
+    auto chunk_off = [&](int row, int c) { return row * ROWB + ((c ^ swz(row)) << 4); };
+    auto quad_off = [&](int row, int kq) {
+        return row * ROWB + (((kq >> 1) ^ swz(row)) << 4) + ((kq & 1) << 3);
+    };
+
+    // tile coordinates: XCD-aware, grouped along M (as the generic kernel)
+    const int64_t tiles_m = (p.M + BM - 1) / BM;
+    const int64_t tiles_n = (p.N + BN - 1) / BN;
+    const int64_t nb = (int64_t)gridDim.x;
+    int64_t bid = blockIdx.x;
+    {
+        const int64_t x = bid & 7, i = bid >> 3, q = nb >> 3, r = nb & 7;
+        bid = x * q + (x < r ? x : r) + i;
+    }
+    constexpr int GM = HEAL_GROUP_M;
+    const int64_t group = bid / (GM * tiles_n);
+    const int64_t first_m = group * GM;
+    const int64_t gm = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
+    const int64_t in_group = bid - group * GM * tiles_n;
+    const int64_t m0 = (first_m + in_group % gm) * BM;
+    const int64_t n0 = (in_group / gm) * BN;
+
+    const int64_t M = p.M, N = p.N, K = p.K;
+    const int ns = (int)((K + BK - 1) / BK);     // stages = packed chunks per column block
+    const int64_t KC = ns;
+    const int64_t NB16 = (N + 15) / 16;
+    const int rows_a = (int)((M - m0) < BM ? (M - m0) : BM);
+    const int blocks_b = (int)((NB16 - n0 / 16) < 16 ? (NB16 - n0 / 16) : 16);
+
+    const int a_row = tid >> 3, a_kq = tid & 7;
+    const int st_a = quad_off(a_row, a_kq);
+    const int rd_a = chunk_off(wm * 64 + fr, fg);
+    const int rd_b = (wn * 8) * O::BP * 1024 + lane * 16;
+
+    for (int64_t b = blockIdx.y; b < p.batch; b += gridDim.y) {
+        const float *A = reinterpret_cast<const float *>(p.A) + b * p.strideA + m0 * p.lda;
+        const char *Bp = reinterpret_cast<const char *>(p.B) + b * p.strideB * 2 +
+                         (n0 / 16) * KC * O::BP * 1024;
+        float *__restrict__ C = p.C + b * p.strideC;
+        // ranges checked on the host to stay below 2^31 bytes
+        const __amdgpu_buffer_rsrc_t ra_src = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(A), (short)0, (int)(((int64_t)(rows_a - 1) * p.lda + K) * 4),
+            kRsrcFlags);
+        const __amdgpu_buffer_rsrc_t rb_src = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<char *>(Bp), (short)0, (int)(blocks_b * KC * O::BP * 1024), kRsrcFlags);
+        uint32_t va[4], vb[NBU];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            va[u] = a_row + 64 * u < rows_a ? (uint32_t)(((a_row + 64 * u) * p.lda + 4 * a_kq) * 4)
+                                            : kOOB;
+        // B unit r = tid + 512v: column block r / (64 BP), plane and lane r % (64 BP)
+#pragma unroll
+        for (int v = 0; v < NBU; ++v) {
+            const int r = tid + NT * v, j = r / (64 * O::BP);
+            vb[v] = j < blocks_b ? (uint32_t)(j * KC * O::BP * 1024 + (r % (64 * O::BP)) * 16)
+                                 : kOOB;
+        }
+
+        f32x4 ra[4];
+        u32x4 rb[NBU];
+        auto load_a = [&](int u, int s) {
+            uint32_t v = va[u];
+            if (TAIL && s * BK + 4 * a_kq >= K) v = kOOB;
+            ra[u] = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra_src, (int)v, s * BK * 4, 0));
+        };
+        auto load_b = [&](int v, int s) {
+            rb[v] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                  rb_src, (int)vb[v], s * O::BP * 1024, 0));
+        };
+        // units 0..3: the A quads, converted; 4..: packed B units, copied
+        auto split_unit = [&](char *st, int u) {
+            if (u < 4) {
+                const float x0 = ra[u].x, x1 = ra[u].y, x2 = ra[u].z, x3 = ra[u].w;
+                const int off = st_a + u * 64 * ROWB;
+                if constexpr (OP == OP_BASE) {
+                    const u32x2 h = {cvt2_f16(x0, x1), cvt2_f16(x2, x3)};
+                    *reinterpret_cast<u32x2 *>(st + off) = h;
+                } else {
+                    uint32_t h0, l0, h1, l1;
+                    if constexpr (OP == OP_FULL) {
+                        split2_f16(x0, x1, h0, l0);
+                        split2_f16(x2, x3, h1, l1);
+                    } else {
+                        split2(x0, x1, h0, l0);
+                        split2(x2, x3, h1, l1);
+                    }
+                    const u32x2 h = {h0, h1}, l = {l0, l1};
+                    *reinterpret_cast<u32x2 *>(st + off) = h;
+                    *reinterpret_cast<u32x2 *>(st + A_PLANE + off) = l;
+                }
+            } else {
+                const int v = u - 4;
+                *reinterpret_cast<u32x4 *>(st + O::AP * A_PLANE + (tid + NT * v) * 16) = rb[v];
+            }
+        };
+        auto reload_unit = [&](int u, int s) {
+            if (u < 4) load_a(u, s);
+            else load_b(u - 4, s);
+        };
+
+        f32x4 acc[8][4];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+        if (ns > 0) {
+#pragma unroll
+            for (int u = 0; u < NU; ++u) reload_unit(u, 0);
+#pragma unroll
+            for (int u = 0; u < NU; ++u) split_unit(smem, u);
+            const int s1 = ns > 1 ? 1 : 0;
+#pragma unroll
+            for (int u = 0; u < NU; ++u) reload_unit(u, s1);
+            __syncthreads();
+        }
+
+        for (int s = 0; s < ns; ++s) {
+            const char *cur = smem + (s & 1) * STAGE;
+            char *nxt = smem + ((s + 1) & 1) * STAGE;
+            const int s_reload = s + 2 < ns ? s + 2 : ns - 1;
+            const char *a_hi = cur, *a_lo = cur + A_PLANE, *bw = cur + O::AP * A_PLANE;
+            u32x4 ah[4], al[4], bh[2], bl[2];
+            bh[0] = *reinterpret_cast<const u32x4 *>(bw + rd_b);
+            if (O::BP == 2) bl[0] = *reinterpret_cast<const u32x4 *>(bw + rd_b + 1024);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                ah[i] = *reinterpret_cast<const u32x4 *>(a_hi + rd_a + i * 16 * ROWB);
+            if (O::AP == 2) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    al[i] = *reinterpret_cast<const u32x4 *>(a_lo + rd_a + i * 16 * ROWB);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int c = j & 1;
+                if (j + 1 < 8) {
+                    const int off = rd_b + (j + 1) * O::BP * 1024;
+                    bh[c ^ 1] = *reinterpret_cast<const u32x4 *>(bw + off);
+                    if (O::BP == 2) bl[c ^ 1] = *reinterpret_cast<const u32x4 *>(bw + off + 1024);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[j][i] = mma<BF16>(bh[c], ah[i], acc[j][i]);
+                if (j < NU) {
+                    split_unit(nxt, j);
+                    reload_unit(j, s_reload);
+                }
+                if constexpr (OP == OP_FULL) {
+                    // the weight fragment scaled by 2^-10 for the residual product
+                    const u32x4 bs = __builtin_bit_cast(
+                        u32x4, __builtin_bit_cast(f16x8, bh[c]) * (_Float16)0x1p-10f);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[j][i] = mma<false>(bs, al[i], acc[j][i]);
+                } else if constexpr (OP == OP_PRESPLIT) {
+                    // hiA*hiB, hiA*loB, loA*hiB: the order of heal_gemm_f32
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[j][i] = mma<true>(bl[c], ah[i], acc[j][i]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[j][i] = mma<true>(bh[c], al[i], acc[j][i]);
+                }
+                // one column block: fragment reads, then MFMAs interleaved with
+                // the conversion's VALU work, LDS writes and the reloads
+                __builtin_amdgcn_sched_group_barrier(0x100, O::BP, 0);
+#pragma unroll
+                for (int t = 0; t < MF - 2; ++t) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, MF == 4 ? 4 : 3, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            __syncthreads();
+        }
+
+        // epilogue: FP32 C (2^-e acc for the FP16 forms), streaming stores
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t m = m0 + wm * 64 + i * 16 + fr;
+                const int64_t n = n0 + wn * 128 + j * 16 + 4 * fg;
+                f32x4 v;
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    v[t] = OP == OP_PRESPLIT ? acc[j][i][t] : ldexpf(acc[j][i][t], -p.e);
+                if (m < M && n < N) {
+                    float *cp = C + m * p.ldc + n;
+                    if (p.vecC && n + 4 <= N) {
+                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(cp));
+                    } else {
+                        cp[0] = v.x;
+                        if (n + 1 < N) cp[1] = v.y;
+                        if (n + 2 < N) cp[2] = v.z;
+                        if (n + 3 < N) cp[3] = v.w;
+                    }
+                }
+            }
+        }
+        if (b + gridDim.y < p.batch) __syncthreads();  // LDS reuse by the next batch entry
+    }
+}
+
+// Whether the hand-scheduled kernel can run the call: 16-byte A rows, whole
+// quads along K, and every buffer range below 2^31 bytes.
+template <int OP>
+bool op8_applies(const OpArgs &a)
+{
+    const int64_t lim = 0x7fffffffLL;
+    if (!a.vecA || a.K % 4 != 0) return false;
+    if (((int64_t)255 * a.lda + a.K) * 4 >= lim) return false;
+    const int64_t KC = (a.K + 31) / 32;
+    if (16 * KC * OpT<OP>::BP * 1024 >= lim) return false;
+    return (a.M + 255) / 256 * ((a.N + 255) / 256) <= lim;
+}
+
+template <int OP>
+hipError_t launch_op8(const OpArgs &a, hipStream_t stream)
+{
+    const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
+    const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
+    const dim3 grid((unsigned)tiles, gy);
+    if (a.K % 32)
+        hipLaunchKernelGGL((gemm_op8_kernel<OP, true>), grid, dim3(512), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm_op8_kernel<OP, false>), grid, dim3(512), 0, stream, a);
+    return hipGetLastError();
+}
+
 // Whether the 16-byte buffer-load path can run the call: rows aligned, whole
 // 16-byte units along K, and every byte offset inside a tile below 2^31.
 // (Packed B is always read with buffer loads; the caller bounds K so that a
@@ -618,8 +891,11 @@ hipError_t launch_large(const OpArgs &a, hipStream_t stream)
     if constexpr (OP == OP_SCORES) {
         return launch_cfg<OP, HEAL_OP_LARGE_CFG>(a, stream);
     } else {
+        // the hand-scheduled kernel wherever it applies (it beats the generic
+        // 224-column tiles also where those need fewer rounds)
+        if (HEAL_OP_LARGE8 && op8_applies<OP>(a)) return launch_op8<OP>(a, stream);
         const int cus = device_cus();
-        const bool n224 = large_cost(a, 224, cus) < large_cost(a, 256, cus);
+        const bool n224 = HEAL_OP_N224 && large_cost(a, 224, cus) < large_cost(a, 256, cus);
         if constexpr (OP == OP_FULL)
             return n224 ? launch_cfg<OP, HEAL_OP_LARGE_FULL_N224_CFG>(a, stream)
                         : launch_cfg<OP, HEAL_OP_LARGE_FULL_CFG>(a, stream);

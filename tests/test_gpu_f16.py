@@ -198,7 +198,8 @@ def _rows(M, n, seed):
     return np.array(sorted(r), dtype=np.int64)
 
 
-@pytest.mark.parametrize("name,nrows", [("decode", 16), ("prefill_up", 4), ("lm_head", 3)])
+@pytest.mark.parametrize("name,nrows", [("decode", 16), ("prefill_up", 4), ("lm_head", 3),
+                                        ("square8192", 3)])
 def test_f16w_workloads_sampled(orc, name, nrows):
     """The linear-layer workloads at full size, W = B^T (a linear layer's N x K
     weight), both forms, sampled rows against the oracle."""
@@ -266,7 +267,7 @@ def _large_widths_shapes():
     return [wide, narrow]
 
 
-@pytest.mark.parametrize("K", [72, 37])
+@pytest.mark.parametrize("K", [72, 37, 96])
 def test_large_tile_widths(orc, K):
     """Both tile widths of the large instance: the whole output bitwise equal
     to the medium instance (and, pre-split, to heal_gemm_f32), sampled rows
@@ -321,7 +322,7 @@ def test_presplit_bitwise_equal(orc, instance, shape):
     assert torch.equal(Bpt, Bp), "packing of the transposed storage differs"
 
 
-@pytest.mark.parametrize("name", ["decode", "lm_head", "prefill_up"])
+@pytest.mark.parametrize("name", ["decode", "lm_head", "prefill_up", "square8192"])
 def test_presplit_workloads_bitwise(name):
     w = wl.WORKLOADS[name]
     A, B = wl.make_inputs(w)
