@@ -52,13 +52,26 @@ constexpr int kPlane = 256 * kRowB;     // 16 KB
 constexpr int kStage = 4 * kPlane;      // A_hi, A_lo, B_hi, B_lo
 constexpr uint32_t kOOB = 0x80000000u;  // buffer offset beyond every range: reads 0
 
-// Instruction interleave of one 24-MFMA group (tuning knobs).
+// Tuning knobs.  Waves per workgroup: 8, or 4 for the one-wave-per-SIMD form.
 #ifndef HEAL_LARGE_WAVES
 #define HEAL_LARGE_WAVES 8
 #endif
+// Instruction pattern of one 12-MFMA column block of the 8-wave form:
+// 1: fragment reads, 6 x (MFMA, 2 VALU), LDS writes, reloads, 6 MFMAs;
+// 2: 12 x (MFMA, VALU); 3: 10 x (MFMA, 3 VALU), then the rest;
+// 4 (default): fragment reads, HEAL_L8_NV x (MFMA, HEAL_L8_VPM VALU), LDS
+// writes, reloads, the remaining MFMAs (8 x 2: 1.1-1.3% faster than 1 at
+// 8192^3 on two boards; 7, 9 pairs or 3 VALU per MFMA were not).
 #ifndef HEAL_L8_PATTERN
-#define HEAL_L8_PATTERN 1
+#define HEAL_L8_PATTERN 4
 #endif
+#ifndef HEAL_L8_NV
+#define HEAL_L8_NV 8
+#endif
+#ifndef HEAL_L8_VPM
+#define HEAL_L8_VPM 2
+#endif
+// 4-wave form: VALU slots of one 24-MFMA group, and VALU per slot.
 #ifndef HEAL_LARGE_VALU_SLOTS
 #define HEAL_LARGE_VALU_SLOTS 12
 #endif
@@ -546,6 +559,26 @@ gemm_large8_kernel(GemmArgs p)
                 }
                 __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
                 __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+#elif HEAL_L8_PATTERN == 3
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+                for (int t = 0; t < 10; ++t) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+#elif HEAL_L8_PATTERN == 4
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+                for (int t = 0; t < HEAL_L8_NV; ++t) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, HEAL_L8_VPM, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 12 - HEAL_L8_NV, 0);
 #endif
                 __builtin_amdgcn_sched_barrier(0);
             }
