@@ -521,6 +521,19 @@ gemm_op8_kernel(OpArgs p)
     constexpr int NU = 4 + NBU;                  // conversion units per thread and stage
     constexpr int MF = 4 * (OP == OP_BASE ? 1 : OP == OP_FULL ? 2 : 3);  // MFMAs per column block
     static_assert(NU <= 8, "one unit per column block");
+    // instruction pattern per column block: NV x (MFMA, VPM VALU), then the
+    // rest (measured at 8192^3: 8 x 2 for the pre-split product, 1.1% faster
+    // than 10 x 3; 6 x 2 for HEAL-Full, within 0.5% of 6 x 3; HEAL-Base flat)
+#ifdef HEAL_OP8_NV
+    constexpr int NV = HEAL_OP8_NV < MF ? HEAL_OP8_NV : MF - 1;
+#else
+    constexpr int NV = MF == 12 ? 8 : MF - 2;
+#endif
+#ifdef HEAL_OP8_VPM
+    constexpr int VPM = HEAL_OP8_VPM;
+#else
+    constexpr int VPM = MF == 4 ? 4 : 2;
+#endif
     static_assert(2 * STAGE <= 160 * 1024, "two LDS stages must fit the 160 KB of a CU");
     __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
 
@@ -695,13 +708,13 @@ gemm_op8_kernel(OpArgs p)
                 // the conversion's VALU work, LDS writes and the reloads
                 __builtin_amdgcn_sched_group_barrier(0x100, O::BP, 0);
 #pragma unroll
-                for (int t = 0; t < MF - 2; ++t) {
+                for (int t = 0; t < NV; ++t) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x002, MF == 4 ? 4 : 3, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);
                 }
                 __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
                 __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, MF - NV, 0);
                 __builtin_amdgcn_sched_barrier(0);
             }
             __syncthreads();
