@@ -506,6 +506,12 @@ gemm_op_kernel(OpArgs p)
 #define HEAL_OP_N224 1
 #endif
 
+// Stage depth in 32-deep chunks: HEAL-Base takes two per barrier (its single
+// product leaves one chunk's MFMAs too short against the barrier).
+#ifndef HEAL_OP8_BASE_KS
+#define HEAL_OP8_BASE_KS 2
+#endif
+
 template <int OP, bool TAIL>
 __global__ void __launch_bounds__(512, 1)
 gemm_op8_kernel(OpArgs p)
@@ -513,14 +519,20 @@ gemm_op8_kernel(OpArgs p)
     using O = OpT<OP>;
     static_assert(!O::A_I16 && !O::B_ROWS, "packed-weight products only");
     constexpr bool BF16 = OP == OP_PRESPLIT;
-    constexpr int NT = 512, BM = 256, BN = 256, BK = 32, ROWB = 2 * BK;
-    constexpr int A_PLANE = BM * ROWB;           // 16 KB per 16-bit plane of A
-    constexpr int B_BYTES = (BN / 16) * O::BP * 1024;  // 16 column blocks, fragment order
+    constexpr int KS = OP == OP_BASE ? HEAL_OP8_BASE_KS : 1;   // 32-deep chunks per stage
+    constexpr int NT = 512, BM = 256, BN = 256, BK = 32 * KS, ROWB = 2 * BK;
+    constexpr int KQ = BK / 4;                   // k-quads per A row and stage
+    constexpr int RPW = BK >= 64 ? 1 : 64 / BK;  // rows sharing one 128-byte window
+    constexpr int SWM = (BK / 8 < 8 ? BK / 8 : 8) - 1;
+    constexpr int A_PLANE = BM * ROWB;           // one 16-bit plane of A
+    constexpr int B_BYTES = (BN / 16) * KS * O::BP * 1024;  // 16 column blocks, fragment order
     constexpr int STAGE = O::AP * A_PLANE + B_BYTES;
-    constexpr int NBU = 2 * O::BP;               // B units per thread and stage
-    constexpr int NU = 4 + NBU;                  // conversion units per thread and stage
+    constexpr int NAU = BM * KQ / NT;            // A quads per thread and stage
+    constexpr int NBU = 2 * KS * O::BP;          // B units per thread and stage
+    constexpr int NU = NAU + NBU;                // conversion units per thread and stage
     constexpr int MF = 4 * (OP == OP_BASE ? 1 : OP == OP_FULL ? 2 : 3);  // MFMAs per column block
-    static_assert(NU <= 8, "one unit per column block");
+    static_assert(NAU * NT == BM * KQ, "whole A quads per thread");
+    static_assert(NU <= 8 * KS, "one unit per column block and chunk");
     // instruction pattern per column block: NV x (MFMA, VPM VALU), then the
     // rest (measured at 8192^3: 8 x 2 for the pre-split product, 1.1% faster
     // than 10 x 3; 6 x 2 for HEAL-Full, within 0.5% of 6 x 3; HEAL-Base flat)
@@ -542,7 +554,7 @@ gemm_op8_kernel(OpArgs p)
     const int wave = tid >> 6;
     const int wm = wave & 3, wn = wave >> 2;
     const int fr = lane & 15, fg = lane >> 4;
-    auto swz = [](int row) { return (row >> 1) & 3; };
+    auto swz = [](int row) { return (row / RPW) & SWM; };
     auto chunk_off = [&](int row, int c) { return row * ROWB + ((c ^ swz(row)) << 4); };
     auto quad_off = [&](int row, int kq) {
         return row * ROWB + (((kq >> 1) ^ swz(row)) << 4) + ((kq & 1) << 3);
@@ -566,16 +578,25 @@ gemm_op8_kernel(OpArgs p)
     const int64_t n0 = (in_group / gm) * BN;
 
     const int64_t M = p.M, N = p.N, K = p.K;
-    const int ns = (int)((K + BK - 1) / BK);     // stages = packed chunks per column block
-    const int64_t KC = ns;
+    const int ns = (int)((K + BK - 1) / BK);     // stages
+    const int64_t KC = (K + 31) / 32;            // packed chunks per column block
     const int64_t NB16 = (N + 15) / 16;
     const int rows_a = (int)((M - m0) < BM ? (M - m0) : BM);
     const int blocks_b = (int)((NB16 - n0 / 16) < 16 ? (NB16 - n0 / 16) : 16);
 
-    const int a_row = tid >> 3, a_kq = tid & 7;
-    const int st_a = quad_off(a_row, a_kq);
-    const int rd_a = chunk_off(wm * 64 + fr, fg);
-    const int rd_b = (wn * 8) * O::BP * 1024 + lane * 16;
+    // A quad u of this thread: q = tid + 512u -> row q / KQ, k-quad q % KQ
+    const int a_kq = tid % KQ;
+    int st_a[NAU], a_rw[NAU];
+#pragma unroll
+    for (int u = 0; u < NAU; ++u) {
+        a_rw[u] = (tid + NT * u) / KQ;
+        st_a[u] = quad_off(a_rw[u], a_kq);
+    }
+    // B unit v: r = tid + 512v -> column block r / (64 KS BP), then chunk,
+    // plane and lane (the packed order within a block)
+    int b_kc[NBU];
+#pragma unroll
+    for (int v = 0; v < NBU; ++v) b_kc[v] = ((tid + NT * v) % (64 * KS * O::BP)) / (64 * O::BP);
 
     for (int64_t b = blockIdx.y; b < p.batch; b += gridDim.y) {
         const float *A = reinterpret_cast<const float *>(p.A) + b * p.strideA + m0 * p.lda;
@@ -588,20 +609,19 @@ gemm_op8_kernel(OpArgs p)
             kRsrcFlags);
         const __amdgpu_buffer_rsrc_t rb_src = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<char *>(Bp), (short)0, (int)(blocks_b * KC * O::BP * 1024), kRsrcFlags);
-        uint32_t va[4], vb[NBU];
+        uint32_t va[NAU], vb[NBU];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            va[u] = a_row + 64 * u < rows_a ? (uint32_t)(((a_row + 64 * u) * p.lda + 4 * a_kq) * 4)
-                                            : kOOB;
-        // B unit r = tid + 512v: column block r / (64 BP), plane and lane r % (64 BP)
+        for (int u = 0; u < NAU; ++u)
+            va[u] = a_rw[u] < rows_a ? (uint32_t)((a_rw[u] * p.lda + 4 * a_kq) * 4) : kOOB;
 #pragma unroll
         for (int v = 0; v < NBU; ++v) {
-            const int r = tid + NT * v, j = r / (64 * O::BP);
-            vb[v] = j < blocks_b ? (uint32_t)(j * KC * O::BP * 1024 + (r % (64 * O::BP)) * 16)
-                                 : kOOB;
+            const int r = tid + NT * v, j = r / (64 * KS * O::BP);
+            vb[v] = j < blocks_b
+                        ? (uint32_t)(j * KC * O::BP * 1024 + (r % (64 * KS * O::BP)) * 16)
+                        : kOOB;
         }
 
-        f32x4 ra[4];
+        f32x4 ra[NAU];
         u32x4 rb[NBU];
         auto load_a = [&](int u, int s) {
             uint32_t v = va[u];
@@ -610,14 +630,17 @@ gemm_op8_kernel(OpArgs p)
                 f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra_src, (int)v, s * BK * 4, 0));
         };
         auto load_b = [&](int v, int s) {
+            uint32_t o = vb[v];
+            // a stage reaching past the last packed chunk (K tail, KS > 1)
+            if (TAIL && KS > 1 && s * KS + b_kc[v] >= KC) o = kOOB;
             rb[v] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                  rb_src, (int)vb[v], s * O::BP * 1024, 0));
+                                                  rb_src, (int)o, s * KS * O::BP * 1024, 0));
         };
-        // units 0..3: the A quads, converted; 4..: packed B units, copied
+        // units 0..NAU-1: the A quads, converted; then packed B units, copied
         auto split_unit = [&](char *st, int u) {
-            if (u < 4) {
+            if (u < NAU) {
                 const float x0 = ra[u].x, x1 = ra[u].y, x2 = ra[u].z, x3 = ra[u].w;
-                const int off = st_a + u * 64 * ROWB;
+                const int off = st_a[u];
                 if constexpr (OP == OP_BASE) {
                     const u32x2 h = {cvt2_f16(x0, x1), cvt2_f16(x2, x3)};
                     *reinterpret_cast<u32x2 *>(st + off) = h;
@@ -635,13 +658,13 @@ gemm_op8_kernel(OpArgs p)
                     *reinterpret_cast<u32x2 *>(st + A_PLANE + off) = l;
                 }
             } else {
-                const int v = u - 4;
+                const int v = u - NAU;
                 *reinterpret_cast<u32x4 *>(st + O::AP * A_PLANE + (tid + NT * v) * 16) = rb[v];
             }
         };
         auto reload_unit = [&](int u, int s) {
-            if (u < 4) load_a(u, s);
-            else load_b(u - 4, s);
+            if (u < NAU) load_a(u, s);
+            else load_b(u - NAU, s);
         };
 
         f32x4 acc[8][4];
@@ -666,56 +689,62 @@ gemm_op8_kernel(OpArgs p)
             char *nxt = smem + ((s + 1) & 1) * STAGE;
             const int s_reload = s + 2 < ns ? s + 2 : ns - 1;
             const char *a_hi = cur, *a_lo = cur + A_PLANE, *bw = cur + O::AP * A_PLANE;
-            u32x4 ah[4], al[4], bh[2], bl[2];
-            bh[0] = *reinterpret_cast<const u32x4 *>(bw + rd_b);
-            if (O::BP == 2) bl[0] = *reinterpret_cast<const u32x4 *>(bw + rd_b + 1024);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                ah[i] = *reinterpret_cast<const u32x4 *>(a_hi + rd_a + i * 16 * ROWB);
-            if (O::AP == 2) {
+            for (int kc = 0; kc < KS; ++kc) {
+                // column block j of chunk kc: (wn*8 + j) KS BP KiB + kc BP KiB
+                const int rd_b = ((wn * 8) * KS + kc) * O::BP * 1024 + lane * 16;
+                const int rd_a = chunk_off(wm * 64 + fr, kc * 4 + fg);
+                u32x4 ah[4], al[4], bh[2], bl[2];
+                bh[0] = *reinterpret_cast<const u32x4 *>(bw + rd_b);
+                if (O::BP == 2) bl[0] = *reinterpret_cast<const u32x4 *>(bw + rd_b + 1024);
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    al[i] = *reinterpret_cast<const u32x4 *>(a_lo + rd_a + i * 16 * ROWB);
-            }
+                    ah[i] = *reinterpret_cast<const u32x4 *>(a_hi + rd_a + i * 16 * ROWB);
+                if (O::AP == 2) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int c = j & 1;
-                if (j + 1 < 8) {
-                    const int off = rd_b + (j + 1) * O::BP * 1024;
-                    bh[c ^ 1] = *reinterpret_cast<const u32x4 *>(bw + off);
-                    if (O::BP == 2) bl[c ^ 1] = *reinterpret_cast<const u32x4 *>(bw + off + 1024);
+                    for (int i = 0; i < 4; ++i)
+                        al[i] = *reinterpret_cast<const u32x4 *>(a_lo + rd_a + i * 16 * ROWB);
                 }
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[j][i] = mma<BF16>(bh[c], ah[i], acc[j][i]);
-                if (j < NU) {
-                    split_unit(nxt, j);
-                    reload_unit(j, s_reload);
+                for (int j = 0; j < 8; ++j) {
+                    const int c = j & 1, slot = kc * 8 + j;
+                    if (j + 1 < 8) {
+                        const int off = rd_b + (j + 1) * KS * O::BP * 1024;
+                        bh[c ^ 1] = *reinterpret_cast<const u32x4 *>(bw + off);
+                        if (O::BP == 2) bl[c ^ 1] = *reinterpret_cast<const u32x4 *>(bw + off + 1024);
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[j][i] = mma<BF16>(bh[c], ah[i], acc[j][i]);
+                    if (slot < NU) {
+                        split_unit(nxt, slot);
+                        reload_unit(slot, s_reload);
+                    }
+                    if constexpr (OP == OP_FULL) {
+                        // the weight fragment scaled by 2^-10 for the residual product
+                        const u32x4 bs = __builtin_bit_cast(
+                            u32x4, __builtin_bit_cast(f16x8, bh[c]) * (_Float16)0x1p-10f);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) acc[j][i] = mma<false>(bs, al[i], acc[j][i]);
+                    } else if constexpr (OP == OP_PRESPLIT) {
+                        // hiA*hiB, hiA*loB, loA*hiB: the order of heal_gemm_f32
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) acc[j][i] = mma<true>(bl[c], ah[i], acc[j][i]);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) acc[j][i] = mma<true>(bh[c], al[i], acc[j][i]);
+                    }
+                    // one column block: fragment reads, then MFMAs interleaved with
+                    // the conversion's VALU work, LDS writes and the reloads
+                    __builtin_amdgcn_sched_group_barrier(0x100, O::BP, 0);
+#pragma unroll
+                    for (int t = 0; t < NV; ++t) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);
+                    }
+                    __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, MF - NV, 0);
+                    __builtin_amdgcn_sched_barrier(0);
                 }
-                if constexpr (OP == OP_FULL) {
-                    // the weight fragment scaled by 2^-10 for the residual product
-                    const u32x4 bs = __builtin_bit_cast(
-                        u32x4, __builtin_bit_cast(f16x8, bh[c]) * (_Float16)0x1p-10f);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[j][i] = mma<false>(bs, al[i], acc[j][i]);
-                } else if constexpr (OP == OP_PRESPLIT) {
-                    // hiA*hiB, hiA*loB, loA*hiB: the order of heal_gemm_f32
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[j][i] = mma<true>(bl[c], ah[i], acc[j][i]);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[j][i] = mma<true>(bh[c], al[i], acc[j][i]);
-                }
-                // one column block: fragment reads, then MFMAs interleaved with
-                // the conversion's VALU work, LDS writes and the reloads
-                __builtin_amdgcn_sched_group_barrier(0x100, O::BP, 0);
-#pragma unroll
-                for (int t = 0; t < NV; ++t) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);
-                }
-                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
-                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, MF - NV, 0);
-                __builtin_amdgcn_sched_barrier(0);
             }
             __syncthreads();
         }
@@ -767,7 +796,8 @@ hipError_t launch_op8(const OpArgs &a, hipStream_t stream)
     const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
     const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
     const dim3 grid((unsigned)tiles, gy);
-    if (a.K % 32)
+    const int bk = OP == OP_BASE ? 32 * HEAL_OP8_BASE_KS : 32;
+    if (a.K % bk)
         hipLaunchKernelGGL((gemm_op8_kernel<OP, true>), grid, dim3(512), 0, stream, a);
     else
         hipLaunchKernelGGL((gemm_op8_kernel<OP, false>), grid, dim3(512), 0, stream, a);
