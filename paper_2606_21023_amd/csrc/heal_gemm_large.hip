@@ -59,9 +59,10 @@ constexpr uint32_t kOOB = 0x80000000u;  // buffer offset beyond every range: rea
 // Instruction pattern of one 12-MFMA column block of the 8-wave form:
 // 1: fragment reads, 6 x (MFMA, 2 VALU), LDS writes, reloads, 6 MFMAs;
 // 2: 12 x (MFMA, VALU); 3: 10 x (MFMA, 3 VALU), then the rest;
-// 4 (default): fragment reads, HEAL_L8_NV x (MFMA, HEAL_L8_VPM VALU), LDS
-// writes, reloads, the remaining MFMAs (8 x 2: 1.1-1.3% faster than 1 at
-// 8192^3 on two boards; 7, 9 pairs or 3 VALU per MFMA were not).
+// 4 (default): fragment reads, HEAL_L8_NV x (MFMA, HEAL_L8_VPM VALU), the
+// reloads, the LDS writes, the remaining MFMAs (8 x 2: 1.1-1.3% faster than
+// 1 at 8192^3 on two boards; 7, 9, 10 pairs or 1 or 3 VALU per MFMA were
+// not; reloads before the LDS writes another 0.9-1.3% on two boards).
 #ifndef HEAL_L8_PATTERN
 #define HEAL_L8_PATTERN 4
 #endif
@@ -70,6 +71,9 @@ constexpr uint32_t kOOB = 0x80000000u;  // buffer offset beyond every range: rea
 #endif
 #ifndef HEAL_L8_VPM
 #define HEAL_L8_VPM 2
+#endif
+#ifndef HEAL_L8_VMEM_FIRST
+#define HEAL_L8_VMEM_FIRST 1
 #endif
 // 4-wave form: VALU slots of one 24-MFMA group, and VALU per slot.
 #ifndef HEAL_LARGE_VALU_SLOTS
@@ -576,8 +580,13 @@ gemm_large8_kernel(GemmArgs p)
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                     __builtin_amdgcn_sched_group_barrier(0x002, HEAL_L8_VPM, 0);
                 }
+#if HEAL_L8_VMEM_FIRST
+                __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+#else
                 __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
                 __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+#endif
                 __builtin_amdgcn_sched_group_barrier(0x008, 12 - HEAL_L8_NV, 0);
 #endif
                 __builtin_amdgcn_sched_barrier(0);
