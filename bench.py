@@ -430,8 +430,15 @@ def main():
         label = OP_INSTANCE_NAMES.get(instance, "?")
         kname = "gemm_op_kernel"
         if instance == 1 and method != "i16_scores":
-            # 16-byte aligned rows: the hand-scheduled 256 x 256 kernel
-            kname, label = "gemm_op8_kernel", "large 256x256, 8 waves of 64x128, hand-scheduled"
+            # 16-byte aligned rows: the hand-scheduled kernel, 224 columns
+            # where that takes fewer rounds of one workgroup per CU
+            cus = torch.cuda.get_device_properties(0).multi_processor_count
+            def cost(bn):
+                wgs = -(-w.M // 256) * -(-w.N // bn) * w.batch
+                return -(-wgs // cus) * bn
+            bn = 224 if method != "f16_base" and cost(224) < cost(256) else 256
+            kname = "gemm_op8_kernel"
+            label = "large 256x%d, 8 waves of 64x%d, hand-scheduled" % (bn, bn // 2)
         kernel = "%s<%s> (%s)" % (kname, method, label)
     mfma_dtype = "bf16" if meta["products"] == 3 else "f16"
     if t_mfma >= t_hbm:

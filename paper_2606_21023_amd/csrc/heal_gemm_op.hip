@@ -508,11 +508,14 @@ gemm_op_kernel(OpArgs p)
 
 // Stage depth in 32-deep chunks: HEAL-Base takes two per barrier (its single
 // product leaves one chunk's MFMAs too short against the barrier).
+#ifndef HEAL_OP8_N224
+#define HEAL_OP8_N224 1
+#endif
 #ifndef HEAL_OP8_BASE_KS
 #define HEAL_OP8_BASE_KS 2
 #endif
 
-template <int OP, bool TAIL>
+template <int OP, int BN, bool TAIL>
 __global__ void __launch_bounds__(512, 1)
 gemm_op8_kernel(OpArgs p)
 {
@@ -520,19 +523,24 @@ gemm_op8_kernel(OpArgs p)
     static_assert(!O::A_I16 && !O::B_ROWS, "packed-weight products only");
     constexpr bool BF16 = OP == OP_PRESPLIT;
     constexpr int KS = OP == OP_BASE ? HEAL_OP8_BASE_KS : 1;   // 32-deep chunks per stage
-    constexpr int NT = 512, BM = 256, BN = 256, BK = 32 * KS, ROWB = 2 * BK;
+    constexpr int NT = 512, BM = 256, BK = 32 * KS, ROWB = 2 * BK;
+    static_assert(BN == 256 || BN == 224, "tile width");
+    constexpr int WB = BN / 32;                  // column blocks per wave (two waves across)
+    constexpr int TB = BN / 16;                  // column blocks per tile
     constexpr int KQ = BK / 4;                   // k-quads per A row and stage
     constexpr int RPW = BK >= 64 ? 1 : 64 / BK;  // rows sharing one 128-byte window
     constexpr int SWM = (BK / 8 < 8 ? BK / 8 : 8) - 1;
     constexpr int A_PLANE = BM * ROWB;           // one 16-bit plane of A
-    constexpr int B_BYTES = (BN / 16) * KS * O::BP * 1024;  // 16 column blocks, fragment order
+    constexpr int B_BYTES = TB * KS * O::BP * 1024;  // the tile's column blocks, fragment order
+    constexpr int B_UNITS = TB * KS * O::BP * 64;   // 16-byte B units per stage
     constexpr int STAGE = O::AP * A_PLANE + B_BYTES;
     constexpr int NAU = BM * KQ / NT;            // A quads per thread and stage
-    constexpr int NBU = 2 * KS * O::BP;          // B units per thread and stage
+    constexpr int NBU = (B_UNITS + NT - 1) / NT; // B units per thread and stage
     constexpr int NU = NAU + NBU;                // conversion units per thread and stage
     constexpr int MF = 4 * (OP == OP_BASE ? 1 : OP == OP_FULL ? 2 : 3);  // MFMAs per column block
     static_assert(NAU * NT == BM * KQ, "whole A quads per thread");
-    static_assert(NU <= 8 * KS, "one unit per column block and chunk");
+    constexpr int NSLOT = WB * KS;               // column blocks x chunks of one stage
+    static_assert(NU <= 2 * NSLOT, "at most two units per column block and chunk");
     // instruction pattern per column block: NV x (MFMA, VPM VALU), then the
     // rest (measured at 8192^3: 8 x 2 for the pre-split product, 1.1% faster
     // than 10 x 3; 6 x 2 for HEAL-Full, within 0.5% of 6 x 3; HEAL-Base flat)
@@ -582,7 +590,7 @@ gemm_op8_kernel(OpArgs p)
     const int64_t KC = (K + 31) / 32;            // packed chunks per column block
     const int64_t NB16 = (N + 15) / 16;
     const int rows_a = (int)((M - m0) < BM ? (M - m0) : BM);
-    const int blocks_b = (int)((NB16 - n0 / 16) < 16 ? (NB16 - n0 / 16) : 16);
+    const int blocks_b = (int)((NB16 - n0 / 16) < TB ? (NB16 - n0 / 16) : TB);
 
     // A quad u of this thread: q = tid + 512u -> row q / KQ, k-quad q % KQ
     const int a_kq = tid % KQ;
@@ -616,7 +624,7 @@ gemm_op8_kernel(OpArgs p)
 #pragma unroll
         for (int v = 0; v < NBU; ++v) {
             const int r = tid + NT * v, j = r / (64 * KS * O::BP);
-            vb[v] = j < blocks_b
+            vb[v] = j < blocks_b && (B_UNITS % NT == 0 || r < B_UNITS)
                         ? (uint32_t)(j * KC * O::BP * 1024 + (r % (64 * KS * O::BP)) * 16)
                         : kOOB;
         }
@@ -659,6 +667,7 @@ gemm_op8_kernel(OpArgs p)
                 }
             } else {
                 const int v = u - NAU;
+                if (B_UNITS % NT != 0 && tid + NT * v >= B_UNITS) return;
                 *reinterpret_cast<u32x4 *>(st + O::AP * A_PLANE + (tid + NT * v) * 16) = rb[v];
             }
         };
@@ -667,9 +676,9 @@ gemm_op8_kernel(OpArgs p)
             else load_b(u - NAU, s);
         };
 
-        f32x4 acc[8][4];
+        f32x4 acc[WB][4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < WB; ++j)
 #pragma unroll
             for (int i = 0; i < 4; ++i) acc[j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
@@ -692,7 +701,7 @@ gemm_op8_kernel(OpArgs p)
 #pragma unroll
             for (int kc = 0; kc < KS; ++kc) {
                 // column block j of chunk kc: (wn*8 + j) KS BP KiB + kc BP KiB
-                const int rd_b = ((wn * 8) * KS + kc) * O::BP * 1024 + lane * 16;
+                const int rd_b = ((wn * WB) * KS + kc) * O::BP * 1024 + lane * 16;
                 const int rd_a = chunk_off(wm * 64 + fr, kc * 4 + fg);
                 u32x4 ah[4], al[4], bh[2], bl[2];
                 bh[0] = *reinterpret_cast<const u32x4 *>(bw + rd_b);
@@ -706,18 +715,23 @@ gemm_op8_kernel(OpArgs p)
                         al[i] = *reinterpret_cast<const u32x4 *>(a_lo + rd_a + i * 16 * ROWB);
                 }
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int c = j & 1, slot = kc * 8 + j;
-                    if (j + 1 < 8) {
+                for (int j = 0; j < WB; ++j) {
+                    const int c = j & 1, slot = kc * WB + j;
+                    if (j + 1 < WB) {
                         const int off = rd_b + (j + 1) * KS * O::BP * 1024;
                         bh[c ^ 1] = *reinterpret_cast<const u32x4 *>(bw + off);
                         if (O::BP == 2) bl[c ^ 1] = *reinterpret_cast<const u32x4 *>(bw + off + 1024);
                     }
 #pragma unroll
                     for (int i = 0; i < 4; ++i) acc[j][i] = mma<BF16>(bh[c], ah[i], acc[j][i]);
-                    if (slot < NU) {
-                        split_unit(nxt, slot);
-                        reload_unit(slot, s_reload);
+                    // unit u goes to slot u, or (more units than slots) to
+                    // slot u * NSLOT / NU
+#pragma unroll
+                    for (int u = 0; u < NU; ++u) {
+                        if ((NU <= NSLOT ? u : u * NSLOT / NU) == slot) {
+                            split_unit(nxt, u);
+                            reload_unit(u, s_reload);
+                        }
                     }
                     if constexpr (OP == OP_FULL) {
                         // the weight fragment scaled by 2^-10 for the residual product
@@ -751,11 +765,11 @@ gemm_op8_kernel(OpArgs p)
 
         // epilogue: FP32 C (2^-e acc for the FP16 forms), streaming stores
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 0; j < WB; ++j) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int64_t m = m0 + wm * 64 + i * 16 + fr;
-                const int64_t n = n0 + wn * 128 + j * 16 + 4 * fg;
+                const int64_t n = n0 + wn * (BN / 2) + j * 16 + 4 * fg;
                 f32x4 v;
 #pragma unroll
                 for (int t = 0; t < 4; ++t)
@@ -787,20 +801,20 @@ bool op8_applies(const OpArgs &a)
     if (((int64_t)255 * a.lda + a.K) * 4 >= lim) return false;
     const int64_t KC = (a.K + 31) / 32;
     if (16 * KC * OpT<OP>::BP * 1024 >= lim) return false;
-    return (a.M + 255) / 256 * ((a.N + 255) / 256) <= lim;
+    return (a.M + 255) / 256 * ((a.N + 223) / 224) <= lim;
 }
 
-template <int OP>
+template <int OP, int BN>
 hipError_t launch_op8(const OpArgs &a, hipStream_t stream)
 {
-    const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
+    const int64_t tiles = ((a.M + 255) / 256) * ((a.N + BN - 1) / BN);
     const unsigned gy = (unsigned)(a.batch < 65535 ? a.batch : 65535);
     const dim3 grid((unsigned)tiles, gy);
     const int bk = OP == OP_BASE ? 32 * HEAL_OP8_BASE_KS : 32;
     if (a.K % bk)
-        hipLaunchKernelGGL((gemm_op8_kernel<OP, true>), grid, dim3(512), 0, stream, a);
+        hipLaunchKernelGGL((gemm_op8_kernel<OP, BN, true>), grid, dim3(512), 0, stream, a);
     else
-        hipLaunchKernelGGL((gemm_op8_kernel<OP, false>), grid, dim3(512), 0, stream, a);
+        hipLaunchKernelGGL((gemm_op8_kernel<OP, BN, false>), grid, dim3(512), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -936,9 +950,13 @@ hipError_t launch_large(const OpArgs &a, hipStream_t stream)
     } else {
         // the hand-scheduled kernel wherever it applies (it beats the generic
         // 224-column tiles also where those need fewer rounds)
-        if (HEAL_OP_LARGE8 && op8_applies<OP>(a)) return launch_op8<OP>(a, stream);
         const int cus = device_cus();
         const bool n224 = HEAL_OP_N224 && large_cost(a, 224, cus) < large_cost(a, 256, cus);
+        // 224-column tiles where they need fewer rounds (prefill_up: HEAL-Full
+        // 1.01x, pre-split 1.02x; HEAL-Base 0.99x, so it keeps 256)
+        if (HEAL_OP_LARGE8 && op8_applies<OP>(a))
+            return n224 && HEAL_OP8_N224 && OP != OP_BASE ? launch_op8<OP, 224>(a, stream)
+                                                          : launch_op8<OP, 256>(a, stream);
         if constexpr (OP == OP_FULL)
             return n224 ? launch_cfg<OP, HEAL_OP_LARGE_FULL_N224_CFG>(a, stream)
                         : launch_cfg<OP, HEAL_OP_LARGE_FULL_CFG>(a, stream);
