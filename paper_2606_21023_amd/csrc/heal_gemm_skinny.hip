@@ -437,7 +437,10 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 // stage depth is the smallest that gives every thread whole 16-byte units
 // of A and B at the tile's row count.  Narrow strips run 512 threads (half
 // blocks of B): 64 rows 33.6 vs 37.6 us with 256, 1 to 32 rows the same or
-// slightly faster.
+// slightly faster.  Wide strips (lm_head, 64 x 128256 x 4096, with 16, 32
+// or 64 rows): 256 columns everywhere, 512 threads where every thread still
+// gets whole A quads: 0.43 / 0.40 / 0.37 ms against 0.55 / 0.45 / 0.39 ms
+// for the earlier 128-column strips at 16 and 32 rows and 256 threads.
 #ifndef HEAL_SKINNY_N1
 #define HEAL_SKINNY_N1 1, 256, 2, 512      // M <= 16, narrow: CB, BK, R, NT
 #endif
@@ -448,13 +451,13 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 #define HEAL_SKINNY_N4 1, 256, 2, 512      // 160 KB of LDS: one workgroup per CU
 #endif
 #ifndef HEAL_SKINNY_W1
-#define HEAL_SKINNY_W1 8, 128, 2, 256      // M <= 16, wide (strips of 16*CB columns)
+#define HEAL_SKINNY_W1 16, 64, 2, 256      // M <= 16, wide (strips of 16*CB columns)
 #endif
 #ifndef HEAL_SKINNY_W2
-#define HEAL_SKINNY_W2 8, 64, 2, 256
+#define HEAL_SKINNY_W2 16, 64, 2, 512
 #endif
 #ifndef HEAL_SKINNY_W4
-#define HEAL_SKINNY_W4 16, 32, 2, 256
+#define HEAL_SKINNY_W4 16, 32, 2, 512
 #endif
 #ifndef HEAL_SKINNY_WIDE_MIN_N
 #define HEAL_SKINNY_WIDE_MIN_N 16384
