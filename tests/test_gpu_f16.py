@@ -340,6 +340,23 @@ def test_presplit_workloads_bitwise(name):
 # ---------------------------------------------------------------------------
 # INT16 codes and dual-FP16 scores
 # ---------------------------------------------------------------------------
+def test_scores_batch_beyond_grid_limit():
+    """INT16 scores with more heads than one grid dimension holds: each head
+    bitwise equal to the same head run alone."""
+    M, N, d, P, batch = 5, 9, 24, 7, 70001
+    rng = np.random.default_rng(77)
+    Q7 = torch.from_numpy(rng.integers(-32767, 32768, size=(P, M, d)).astype(np.int16)).cuda()
+    K7 = torch.from_numpy(rng.integers(-32767, 32768, size=(P, N, d)).astype(np.int16)).cuda()
+    mq = torch.tensor([3.0], device="cuda")
+    mk = torch.tensor([0.5], device="cuda")
+    idx = (torch.arange(batch) % P).cuda()
+    announce("scores batch %d" % batch)
+    ref = heal.heal_scores_i16(Q7, K7, mq, mk, alpha=0.125)
+    S = heal.heal_scores_i16(Q7[idx].contiguous(), K7[idx].contiguous(), mq, mk, alpha=0.125)
+    torch.cuda.synchronize()
+    assert torch.equal(S.view(torch.int32), ref[idx].view(torch.int32))
+
+
 @pytest.mark.parametrize("n,offset", [(1, 0), (7, 1), (4096, 0), (1000003, 2)])
 def test_quantize_bitwise(orc, n, offset):
     announce("quantize n=%d offset=%d" % (n, offset))

@@ -280,6 +280,28 @@ def test_skinny_every_m_bitwise(N, K):
         assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "M=%d differs" % m
 
 
+@pytest.mark.parametrize("K", [8, 7], ids=["k8", "k7"])
+@pytest.mark.parametrize("trans_b", [False, True], ids=["b", "bt"])
+def test_batch_beyond_grid_limit(K, trans_b):
+    """More batch entries than one grid dimension holds (65535 workgroups,
+    two entries per workgroup in the medium instance): every instance walks
+    the extra entries, each entry bitwise equal to the same product run in a
+    batch of its own."""
+    M, N, P, batch = 3, 5, 7, 140001
+    rng = np.random.default_rng(K + 2 * trans_b)
+    A7 = rng.standard_normal((P, M, K)).astype(np.float32)
+    B7 = rng.standard_normal((P, N, K) if trans_b else (P, K, N)).astype(np.float32)
+    idx = torch.arange(batch) % P
+    Ad = to_dev(A7)[idx.cuda()].contiguous()
+    Bd = to_dev(B7)[idx.cuda()].contiguous()
+    for inst in INSTANCES:
+        announce("batch %d %s K=%d trans_b=%d" % (batch, INAME[inst], K, trans_b))
+        ref = heal.heal_gemm_f32_instance(inst, to_dev(A7), to_dev(B7), trans_b=trans_b)
+        C = heal.heal_gemm_f32_instance(inst, Ad, Bd, trans_b=trans_b)
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int32), ref[idx.cuda()].view(torch.int32)), INAME[inst]
+
+
 def test_entry_points_bitwise_equal():
     M, N, K = 200, 300, 333
     A = wl.random_matrix((M, K), seed=31)
