@@ -302,6 +302,41 @@ def test_batch_beyond_grid_limit(K, trans_b):
         assert torch.equal(C.view(torch.int32), ref[idx.cuda()].view(torch.int32)), INAME[inst]
 
 
+@pytest.mark.parametrize("which", ["A", "B", "Bt"])
+def test_operands_spanning_more_than_2gib(orc, which):
+    """Leading dimensions that put operand byte offsets past 2^31, so that the
+    kernels' 32-bit-offset paths have to step aside: every instance bitwise
+    equal to the same product on compact operands, and within the bound of
+    the oracle."""
+    big = (1 << 23) + 32                   # 33.5 MB rows
+    trans_b = which == "Bt"
+    M, N, K = (65, 256, 64) if which == "A" else (300, 256, 72) if which == "B" else (300, 96, 64)
+    A = wl.random_matrix((M, K), seed=91)
+    B = wl.random_matrix((N, K) if trans_b else (K, N), seed=92)
+    Ac, Bc = to_dev(A), to_dev(B)
+    if which == "A":
+        full = torch.zeros((M, big), device="cuda")
+        full[:, :K] = Ac
+        Aw, Bw = full[:, :K], Bc
+    else:
+        rows = B.shape[0]
+        full = torch.zeros((rows, big), device="cuda")
+        full[:, :B.shape[1]] = Bc
+        Aw, Bw = Ac, full[:, :B.shape[1]]
+    assert (Aw.shape[0] - 1) * Aw.stride(0) * 4 >= 2 ** 31 or (Bw.shape[0] - 1) * Bw.stride(0) * 4 >= 2 ** 31
+    _, S = orc.gemm3(A, np.ascontiguousarray(B.T) if trans_b else B)
+    for inst in INSTANCES:
+        announce("operands past 2 GiB: %s %s" % (which, INAME[inst]))
+        C = heal.heal_gemm_f32_instance(inst, Aw, Bw, trans_b=trans_b)
+        C0 = heal.heal_gemm_f32_instance(inst, Ac, Bc, trans_b=trans_b)
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int32), C0.view(torch.int32)), INAME[inst]
+        check_tolerance(C.cpu().numpy(), S,
+                        abs_product(A, np.ascontiguousarray(B.T) if trans_b else B),
+                        "past 2 GiB %s %s" % (which, INAME[inst]))
+    del full
+
+
 def test_entry_points_bitwise_equal():
     M, N, K = 200, 300, 333
     A = wl.random_matrix((M, K), seed=31)
