@@ -340,6 +340,41 @@ def test_presplit_workloads_bitwise(name):
 # ---------------------------------------------------------------------------
 # INT16 codes and dual-FP16 scores
 # ---------------------------------------------------------------------------
+def test_f16w_and_presplit_a_rows_past_2gib(orc):
+    """A leading dimension that puts A's byte offsets past 2^31: every
+    instance of both FP16 forms and of the pre-split product bitwise equal to
+    the same call on a compact A, and the FP16 forms within the oracle
+    bound."""
+    M, N, K = 65, 300, 96
+    big = (1 << 23) + 32
+    A, W = f16w_case(M, N, K, seed=123)
+    Ac = to_dev(A)
+    full = torch.zeros((M, big), device="cuda")
+    full[:, :K] = Ac
+    Aw = full[:, :K]
+    assert (M - 1) * big * 4 >= 2 ** 31
+    e = heal.heal_f16_weight_exponent(float(np.abs(W).max()))
+    W16 = heal.heal_pack_f16_weight(to_dev(W), e)
+    Bd = to_dev(np.ascontiguousarray(W.T))
+    Bp = heal.heal_presplit_b(Bd)
+    for inst in INSTANCES:
+        for products in (1, 2):
+            announce("f16w A past 2 GiB p%d %s" % (products, INAME[inst]))
+            C = heal.heal_gemm_f16w(Aw, W16, N, e, products, instance=inst)
+            C0 = heal.heal_gemm_f16w(Ac, W16, N, e, products, instance=inst)
+            torch.cuda.synchronize()
+            assert torch.equal(C.view(torch.int32), C0.view(torch.int32)), (products, INAME[inst])
+            _, S = orc.gemm_f16w(A, W, e, products)
+            check_tolerance(C.cpu().numpy(), S, f16w_absprod(orc, A, W, e),
+                            "A past 2 GiB p%d %s" % (products, INAME[inst]))
+        announce("presplit A past 2 GiB %s" % INAME[inst])
+        Cp = heal.heal_gemm_f32_presplit(Aw, Bp, N, instance=inst)
+        Cp0 = heal.heal_gemm_f32_presplit(Ac, Bp, N, instance=inst)
+        torch.cuda.synchronize()
+        assert torch.equal(Cp.view(torch.int32), Cp0.view(torch.int32)), INAME[inst]
+    del full
+
+
 def test_scores_batch_beyond_grid_limit():
     """INT16 scores with more heads than one grid dimension holds: each head
     bitwise equal to the same head run alone."""
