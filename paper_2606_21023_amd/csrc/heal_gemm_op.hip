@@ -30,6 +30,11 @@
 //   reads its own 16 bytes of a block, consecutive lanes consecutive
 //   addresses), or B as INT16 rows converted like A;
 //   two LDS stages, one barrier per stage; v_mfma_f32_16x16x32_{f16,bf16}.
+// Two kernels share this data path: the generic template gemm_op_kernel (any
+// tile configuration; the conversion of the next stage follows the MFMAs)
+// and gemm_op8_kernel, the large tiles of the packed-weight products with the
+// conversion interleaved between the MFMAs (used wherever its 16-byte loads
+// apply).
 //
 // Reduction order, identical in every instance of one product (so results
 // are bitwise equal run to run and for every M): K is walked in 32-deep
@@ -488,26 +493,26 @@ gemm_op_kernel(OpArgs p)
     }
 }
 
-// The packed-weight products at 256 x 256 tiles with the schedule of the
-// large bf16x3 kernel: eight waves of 64 x 128, one 32-deep stage per barrier,
-// two LDS stages.  While stage s is multiplied out, each staged register group
-// of stage s+1 is converted into the other LDS buffer between the MFMAs of one
-// column block and at once reloaded with stage s+2.  Per stage and thread:
-// four 16-byte quads of A (rows tid/8 + 64u, k-quad tid%8), converted in the
-// generic kernel's LDS layout (HEAL-Full: the FP16 pair; HEAL-Base: one FP16
-// plane; pre-split: the bf16 pair), and 2 BP 16-byte units of the packed B
-// (units tid + 512v of the tile's 16 column blocks), copied to LDS in fragment
-// order.  Same products in the same order as the generic kernel, so the bits
-// are the same.
+// The packed-weight products (HEAL-Base, HEAL-Full, pre-split) at 256 x BN
+// tiles (BN = 256, or 224 where that needs fewer rounds of workgroups) with
+// the schedule of the large bf16x3 kernel: eight waves of 64 x BN/2, two LDS
+// stages, one barrier per stage of KS 32-deep chunks (KS = 2 for HEAL-Base,
+// whose single product per chunk is short against the barrier; 1 otherwise).
+// While stage s is multiplied out, each staged register group of stage s+1
+// is converted into the other LDS buffer between the MFMAs of one column
+// block and at once reloaded with stage s+2.  Per stage and thread: 4 KS
+// 16-byte quads of A (quad q = tid + 512u: row q / (8 KS), k-quad
+// q % (8 KS)), converted in the generic kernel's LDS layout (HEAL-Full: the
+// FP16 pair; HEAL-Base: one FP16 plane; pre-split: the bf16 pair), and the
+// tile's packed B as 16-byte units r = tid + 512v in packed order (column
+// block, chunk, plane, lane), copied to LDS unchanged.  Same products in the
+// same order as the generic kernel, so the bits are the same.
 #ifndef HEAL_OP_LARGE8
 #define HEAL_OP_LARGE8 1
 #endif
 #ifndef HEAL_OP_N224
 #define HEAL_OP_N224 1
 #endif
-
-// Stage depth in 32-deep chunks: HEAL-Base takes two per barrier (its single
-// product leaves one chunk's MFMAs too short against the barrier).
 #ifndef HEAL_OP8_N224
 #define HEAL_OP8_N224 1
 #endif
