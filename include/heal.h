@@ -62,6 +62,13 @@ const char *heal_status_string(heal_status_t status);
 /* Library version as 10000*major + 100*minor + patch. */
 int heal_version(void);
 
+/* Identity of the sources this library was built from: 16 hex digits of a
+ * SHA-256 over the kernel sources, this header and the compiler flags (a
+ * static string; "unknown" if the build did not supply it).  A caller can
+ * compare it with the same hash of the sources it expects, to refuse a stale
+ * binary. */
+const char *heal_build_id(void);
+
 /*
  * heal_split_f32 -- the operand decomposition on its own (Section 4, GEMM
  * paragraph: the FP32 input is decomposed into a 16-bit head and residual).
@@ -71,8 +78,10 @@ int heal_version(void);
  *         IEEE arithmetic (device, written).
  *   n   : number of elements, n >= 0 (n == 0 is a no-op).
  * The subtraction x - hi is exact, so |x - hi - lo| <= 2^-17 |x| for every
- * finite x that does not round to infinity.  hi and lo must not overlap x or
- * each other.  Non-finite inputs follow IEEE arithmetic: x = +/-inf gives
+ * finite x with 2^-117 <= |x| that does not round to infinity; below 2^-117
+ * lo can fall into bf16's subnormal range (step 2^-133) and the error is at
+ * most 2^-134 in absolute terms.  hi and lo must not overlap x or each
+ * other.  Non-finite inputs follow IEEE arithmetic: x = +/-inf gives
  * hi = x and lo = NaN; a finite x that rounds to infinity gives lo = -/+inf;
  * x = NaN gives NaN for both (payloads unspecified).  Any output of the GEMM
  * that such an element reaches is therefore NaN.
@@ -205,10 +214,17 @@ heal_status_t heal_pack_f16_weight(const float *W, int64_t N, int64_t K, int64_t
 /*
  * heal_gemm_f16w -- FP16 GEMM with FP32 activations and FP32 output:
  *   products == 1 (HEAL-Base):  C = 2^-e * sum_k f16(a) w16
- *   products == 2 (HEAL-Full, Section 4 two-product expansion):
- *       C = 2^-e * (sum_k h_hi w16 + 2^-10 sum_k h_lo w16),
- *       with (h_hi, h_lo) as heal_split_f16; the two sums are separate FP32
- *       accumulators, combined by one fused multiply-add and scaled by 2^-e.
+ *   products == 2 (HEAL-Full, Section 4 two-product expansion
+ *       GEMM(h_hi, W) + GEMM(h_lo / 2^10, W)):
+ *       C = 2^-e * sum_k (h_hi w16 + h_lo f16(w16 2^-10)),
+ *       with (h_hi, h_lo) as heal_split_f16.  Both products go into ONE FP32
+ *       accumulator, per 32-deep chunk the head product and then the
+ *       residual product, and the residual's 2^-10 is applied to the FP16
+ *       weight fragment.  w16 2^-10 is exact for |w16| >= 2^-4, that is for
+ *       every weight above 2^-20 of the largest (the scaled weights reach
+ *       2^15); a smaller weight's w16 2^-10 is rounded to FP16's subnormal
+ *       step 2^-24, which moves its residual term by at most
+ *       2^-25 |h_lo| <= 2^-26 |h| (before the 2^-e scale).
  *   A   : M x K FP32, row stride lda >= max(K, 1);
  *   W16 : packed FP16 weight from heal_pack_f16_weight (same N, K, e);
  *   C   : M x N FP32, row stride ldc >= max(N, 1); written, never read.
@@ -248,12 +264,16 @@ heal_status_t heal_gemm_f32_presplit_instance(int instance, int64_t M, int64_t N
 
 /*
  * heal_quantize_i16 -- INT16 storage of a tensor (Section 4, Q/K/V
- * paragraph): q[i] = Round(32767 x[i] / max|x|), the decision taken in FP32 as
- * inv = 32767 / m, t = x * inv, q = t rounded to nearest, ties to even; every
- * code lies in [-32767, 32767].  m = max|x| is written to *maxabs (device) and
- * is the tensor's dequantisation scale (x ~ q * m / 32767).  An all-zero
- * tensor gives m = 0 and zero codes.  x must be finite.  Two kernels are
- * enqueued (the maximum, then the codes); no host synchronisation.
+ * paragraph): q[i] = Round(32767 x[i] / m), m = max|x|, where Round takes the
+ * real quotient to the nearest integer, ties to even.  The decision is exact
+ * for every finite input and every m > 0 however small (it is taken on the
+ * correctly rounded FP64 quotient of the exact product 32767 x, which cannot
+ * cross a half-integer it does not equal); every code lies in
+ * [-32767, 32767] and the extreme element gets +/-32767.  m is written to
+ * *maxabs (device) and is the tensor's dequantisation scale
+ * (x ~ q * m / 32767).  An all-zero tensor gives m = 0 and zero codes.  x
+ * must be finite.  Two kernels are enqueued (the maximum, then the codes);
+ * no host synchronisation.
  */
 heal_status_t heal_quantize_i16(const float *x, int64_t n, int16_t *q, float *maxabs,
                                 hipStream_t stream);
@@ -262,7 +282,9 @@ heal_status_t heal_quantize_i16(const float *x, int64_t n, int16_t *q, float *ma
  * heal_scores_i16 -- attention scores from INT16 Q and K with the dual-FP16
  * expansion (Section 4, displayed attention expansion):
  *   S_b = f * (Q_hi + Q_lo/2^10)(K_hi + K_lo/2^10)^T,
- *   f = ((maxQ / 32767) * (maxK / 32767)) * alpha, each step in FP32,
+ *   f = alpha * (maxQ / 32767) * (maxK / 32767), the dequantisation of both
+ *       codes, evaluated in FP64 and rounded once to FP32 (a factor below
+ *       2^-126 lands in FP32's subnormal range and loses relative precision),
  * where each code q unpacks exactly into hi = RNE_f16(q) and
  * lo/2^10 = q - hi; all four products are accumulated in FP32 (per 32-deep
  * chunk: hi*hi, hi*lo, lo*hi, lo*lo), so the sum is the integer dot product

@@ -332,21 +332,41 @@ float oracle_maxabs(const float *x, int64_t n)
     return m;
 }
 
-/* INT16 codes of a tensor: q = Round(32767 * x / max|X|).  The decision is
- * taken in FP32 in this order: inv = 32767 / m (one rounding), t = x * inv
- * (one rounding), q = t rounded to the nearest integer, ties to even.  An
- * all-zero tensor (m == 0) gives all-zero codes.  |t| <= 32767 * (1 + 2^-23)
- * so every code lies in [-32767, 32767].  x must be finite.  Writes max|X| to
- * *maxabs. */
+/* INT16 codes of a tensor: q = Round(32767 * x / max|X|), Round taking the
+ * real quotient to the nearest integer, ties to even.
+ *
+ * Evaluated as rint((32767 * x) / m) in FP64, which is that exact rounding:
+ *   - 32767 * x is exact (15 by 24 significant bits);
+ *   - write x = X 2^a with X an integer, |X| < 2^24, 2^a the last place of x;
+ *     |m| >= |x| puts m on the same grid, m = Y 2^a with Y an integer >= |X|;
+ *   - a half-integer n + 1/2 that the quotient t = 32767 X / Y does not equal
+ *     lies at least 1/(2Y) away from it (their difference is an integer over
+ *     2Y), while the one rounding of the FP64 division moves t by at most
+ *     2^-53 |t| < 2^-53 2^15 2^24 / Y = 2^-14 / Y;
+ *   - a quotient that is a half-integer (at most 17 bits) is representable and
+ *     the division returns it exactly, so rint sees the tie and takes the even
+ *     neighbour.
+ * The quotient never exceeds 32767 in magnitude, so no range is lost for any
+ * m, however small.  An all-zero tensor (m == 0) gives all-zero codes.  x
+ * must be finite.  Writes max|X| to *maxabs. */
 void oracle_quantize_i16(const float *x, int64_t n, int16_t *q, float *maxabs)
 {
     float m = oracle_maxabs(x, n);
-    float inv = m > 0.0f ? 32767.0f / m : 0.0f;
     for (int64_t i = 0; i < n; ++i) {
-        float t = x[i] * inv;
-        q[i] = (int16_t)rintf(t);
+        double t = m > 0.0f ? (32767.0 * (double)x[i]) / (double)m : 0.0;
+        q[i] = (int16_t)rint(t);
     }
     *maxabs = m;
+}
+
+/* The dequantisation of the score product: a code q of a tensor with maximum
+ * m stands for q * m / 32767, so the scores of codes qQ, qK are
+ *   alpha * (maxQ / 32767) * (maxK / 32767) * sum_k qQ qK;
+ * this returns the factor in front of the sum, in FP64 (alpha * maxQ is exact,
+ * the rest rounds three times, relative error below 2^-51). */
+double oracle_scores_factor(float maxQ, float maxK, float alpha)
+{
+    return (double)alpha * (double)maxQ * (double)maxK / (32767.0 * 32767.0);
 }
 
 /* The dual-FP16 pair of one INT16 code: hi = f16(q), lo = 2^10 * (q - hi);
@@ -364,7 +384,7 @@ void oracle_unpack_i16(int16_t q, uint16_t *hi, uint16_t *lo)
  *   S_ij = sum_k (Qhi + Qlo/2^10)(Khi + Klo/2^10), the four products in the
  *          order hi*hi, hi*lo, lo*hi, lo*lo, k ascending, in FP64 (exact: every
  *          term is an integer or a multiple of 2^-20 well inside 2^53);
- *   factor = ((maxQ / 32767) * (maxK / 32767)) * alpha, each step in FP32;
+ *   factor = oracle_scores_factor(maxQ, maxK, alpha), in FP64;
  *   C_ij = (float)(factor * S_ij).
  * Rows as in oracle_gemm3.  Returns 0, or -1 on allocation failure. */
 int oracle_scores_i16(int64_t M, int64_t N, int64_t K,
@@ -374,9 +394,7 @@ int oracle_scores_i16(int64_t M, int64_t N, int64_t K,
 {
     int64_t n_out = rows ? n_rows : M;
     if (n_out <= 0 || N <= 0) return 0;
-    float sq = maxQ / 32767.0f, sk = maxK / 32767.0f;
-    float prod = sq * sk;
-    float factor = prod * alpha;
+    double factor = oracle_scores_factor(maxQ, maxK, alpha);
     size_t kk = (size_t)(K > 0 ? K : 1);
     double *kh = (double *)malloc(sizeof(double) * (size_t)N * kk);
     double *kl = (double *)malloc(sizeof(double) * (size_t)N * kk);
@@ -413,7 +431,7 @@ int oracle_scores_i16(int64_t M, int64_t N, int64_t K,
                     for (int64_t k = 0; k < K; ++k)
                         s += qh[k] * bh[k] + qh[k] * bl[k] + ql[k] * bh[k] + ql[k] * bl[k];
                     S[r * N + j] = s;
-                    C[r * N + j] = (float)((double)factor * s);
+                    C[r * N + j] = (float)(factor * s);
                 }
             }
         }

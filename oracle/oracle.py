@@ -65,6 +65,8 @@ class Oracle:
             _i16p, ctypes.c_int64, _i16p, ctypes.c_int64, ctypes.c_float, ctypes.c_float,
             ctypes.c_float, _i64p, ctypes.c_int64, _f64p, _f32p]
         lib.oracle_scores_i16.restype = ctypes.c_int
+        lib.oracle_scores_factor.argtypes = [ctypes.c_float, ctypes.c_float, ctypes.c_float]
+        lib.oracle_scores_factor.restype = ctypes.c_double
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         self.lib = lib
@@ -195,8 +197,15 @@ class Oracle:
         self.lib.oracle_unpack_i16_array(_ptr(q, _i16p), _ptr(hi, _u16p), _ptr(lo, _u16p), q.size)
         return hi, lo
 
+    def scores_factor(self, maxQ, maxK, alpha=1.0):
+        """FP64 factor alpha (maxQ/32767)(maxK/32767) of the INT16 scores."""
+        return float(self.lib.oracle_scores_factor(float(np.float32(maxQ)),
+                                                   float(np.float32(maxK)),
+                                                   float(np.float32(alpha))))
+
     def scores_i16(self, Q, Kt, maxQ, maxK, alpha=1.0, rows=None):
-        """Dual-FP16 scores of INT16 Q (M x d) and K (N x d); ``(C, S)``."""
+        """Dual-FP16 scores of INT16 Q (M x d) and K (N x d); ``(C, S)`` with S
+        the integer dot products of the codes and C = f32(factor * S)."""
         Q = np.ascontiguousarray(Q, dtype=np.int16)
         Kt = np.ascontiguousarray(Kt, dtype=np.int16)
         assert Q.ndim == 2 and Kt.ndim == 2 and Q.shape[1] == Kt.shape[1]

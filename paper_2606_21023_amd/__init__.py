@@ -21,11 +21,12 @@ Functions (names follow the C ABI):
   heal_quantize_i16(x)                -> (codes int16, max|x| 1-element tensor)
   heal_scores_i16(Q, Kt, maxQ, maxK, alpha)  -> dual-FP16 scores of INT16 codes, FP32
   lib()                               -> the raw ctypes library
+  build_id(), check_build()           -> the library's source hash; refuse a stale binary
 """
 import ctypes
 import os
 
-__all__ = ["HealError", "lib", "library_path", "heal_split_f32", "heal_gemm_f32",
+__all__ = ["HealError", "lib", "library_path", "build_id", "check_build", "heal_split_f32", "heal_gemm_f32",
            "heal_gemm_f32_strided_batched", "heal_gemm_f32_instance", "select_instance",
            "INSTANCE_AUTO", "INSTANCE_LARGE", "INSTANCE_MEDIUM", "INSTANCE_SKINNY", "STATUS",
            "heal_split_f16", "heal_packed_size", "heal_maxabs_f32", "heal_f16_weight_exponent",
@@ -66,6 +67,8 @@ def lib():
     L.heal_status_string.restype = ctypes.c_char_p
     L.heal_version.argtypes = []
     L.heal_version.restype = ctypes.c_int
+    L.heal_build_id.argtypes = []
+    L.heal_build_id.restype = ctypes.c_char_p
     L.heal_split_f32.argtypes = [_vp, _vp, _vp, _i64, _vp]
     L.heal_split_f32.restype = ctypes.c_int
     L.heal_gemm_f32.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, _i64, _i64, _i64, _vp]
@@ -107,6 +110,22 @@ def lib():
     L.heal_scores_i16.restype = _c
     _lib = L
     return L
+
+
+def build_id():
+    """The source hash the loaded ``libheal.so`` was built from."""
+    return lib().heal_build_id().decode()
+
+
+def check_build():
+    """Raise ``HealError`` unless the loaded ``libheal.so`` was built from the
+    sources beside it (a stale binary would test old code)."""
+    from . import build as _build
+    want, got = _build.source_hash(), build_id()
+    if got != want:
+        raise HealError("libheal.so was built from other sources (build id %s, sources %s); "
+                        "rebuild with `python -m paper_2606_21023_amd.build`" % (got, want))
+    return got
 
 
 def _check(status, what):

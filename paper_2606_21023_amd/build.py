@@ -4,6 +4,7 @@
 root and the library to ``paper_2606_21023_amd/libheal.so``.
 """
 import concurrent.futures as cf
+import hashlib
 import os
 import subprocess
 import sys
@@ -26,10 +27,28 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-I", INCLUDE, "-I", CSRC]
 
 
-def _compile(src):
+def source_hash():
+    """Hash of everything the library is built from: every file under csrc/,
+    the public header and the compiler flags (16 hex digits).  The built
+    library returns the value it was built with from heal_build_id()."""
+    h = hashlib.sha256()
+    files = sorted(f for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp", ".h")))
+    for name in files:
+        h.update(name.encode() + b"\0")
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read() + b"\0")
+    with open(os.path.join(INCLUDE, "heal.h"), "rb") as f:
+        h.update(f.read() + b"\0")
+    flags = [f for f in FLAGS if f not in ("-I", INCLUDE, CSRC)]  # paths differ by machine
+    h.update(" ".join(flags + SOURCES).encode())
+    return h.hexdigest()[:16]
+
+
+def _compile(src, build_id):
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
     lang = ["-x", "hip"] if src.endswith(".cpp") else []
-    cmd = [HIPCC, *FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+    ident = ['-DHEAL_BUILD_ID="%s"' % build_id] if src == "heal_api.cpp" else []
+    cmd = [HIPCC, *FLAGS, *ident, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr))
@@ -39,8 +58,9 @@ def _compile(src):
 def build(verbose=False):
     """Compile every source and link ``libheal.so``; returns its path."""
     os.makedirs(OBJDIR, exist_ok=True)
+    build_id = source_hash()
     with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        objs = list(ex.map(lambda src: _compile(src, build_id), SOURCES))
     tmp = LIBRARY + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -161,6 +161,11 @@ const char *heal_status_string(heal_status_t status)
 
 int heal_version(void) { return 100; }
 
+#ifndef HEAL_BUILD_ID
+#define HEAL_BUILD_ID "unknown"
+#endif
+const char *heal_build_id(void) { return HEAL_BUILD_ID; }
+
 heal_status_t heal_split_f32(const float *x, uint16_t *hi, uint16_t *lo, int64_t n,
                              hipStream_t stream)
 {
@@ -242,14 +247,17 @@ heal_status_t heal_maxabs_f32(const float *x, int64_t rows, int64_t cols, int64_
 heal_status_t heal_f16_weight_exponent(float maxabs, int32_t *e)
 {
     if (!e || !(maxabs >= 0.0f) || maxabs > 3.4028235e38f) return HEAL_ERR_INVALID_VALUE;
-    int32_t r = 0;
-    if (maxabs > 0.0f) {
-        // largest r with maxabs * 2^r <= 65504 (exact in double)
-        const double m = (double)maxabs;
-        while (ldexp(m, r) > 65504.0) --r;
-        while (ldexp(m, r + 1) <= 65504.0) ++r;
+    if (maxabs == 0.0f) {
+        *e = 0;
+        return HEAL_OK;
     }
-    *e = r;
+    // maxabs = f * 2^E with f in [1/2, 1), and 65504 = (1 - 2^-11) * 2^16.
+    // If f <= 1 - 2^-11, then f * 2^16 <= 65504 while f * 2^17 >= 2^16 does
+    // not fit: the exponent is 16 - E.  Otherwise f * 2^16 > 65504 and
+    // f * 2^15 < 2^15 fits: it is 15 - E.
+    int E = 0;
+    const float f = frexpf(maxabs, &E);
+    *e = (f <= 1.0f - 0x1p-11f ? 16 : 15) - E;
     return HEAL_OK;
 }
 

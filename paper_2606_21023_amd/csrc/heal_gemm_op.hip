@@ -17,7 +17,8 @@
 //   OP_SCORES   HEAL+ score product (Section 4, Q/K/V paragraph and its
 //               attention expansion): INT16 codes of Q and K are unpacked into
 //               dual-FP16 pairs and all four products are accumulated:
-//               C = ((maxQ/32767)(maxK/32767) alpha) * sum_k qQ qK.
+//               C = f * sum_k qQ qK, f = alpha (maxQ/32767)(maxK/32767)
+//               computed in FP64 and rounded once to FP32.
 //   OP_PRESPLIT the bf16x3 compensated product of heal_gemm_f32 with B already
 //               split into bf16 (hi, lo) and packed: the same MFMAs in the same
 //               order, so the result is bitwise equal to heal_gemm_f32.
@@ -453,9 +454,9 @@ gemm_op_kernel(OpArgs p)
         // ---- epilogue: FP32 accumulators -> FP32 C, no downcast -----------
         float factor = 1.0f;
         if constexpr (OP == OP_SCORES) {
-            const float sq = *p.maxA / 32767.0f, sk = *p.maxB / 32767.0f;
-            const float prod = sq * sk;
-            factor = prod * p.alpha;
+            // alpha (maxQ / 32767)(maxK / 32767) evaluated in FP64, rounded once
+            factor = (float)((double)p.alpha * (double)*p.maxA * (double)*p.maxB /
+                             (32767.0 * 32767.0));
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {

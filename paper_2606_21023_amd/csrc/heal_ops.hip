@@ -169,15 +169,30 @@ maxabs_kernel(const float *__restrict__ x, int64_t rows, int64_t cols, int64_t l
     }
 }
 
-// INT16 codes q = Round(32767 x / m), m = max|X| read from *maxabs: the
-// decision is taken in FP32 as inv = 32767 / m, t = x * inv, q = t rounded to
-// nearest, ties to even (m = 0 gives inv = 0 and all-zero codes).
+// INT16 code of one element: the real quotient 32767 x / m rounded to the
+// nearest integer, ties to even.  32767 x is exact in FP64, and one correctly
+// rounded FP64 division cannot carry a quotient across a half-integer it does
+// not equal: with x and m on the grid of x's last place 2^a (|m| >= |x|), a
+// half-integer other than the quotient is at least 2^a / (2 |m|) away, the
+// division's error at most 2^-53 * 32767 |x| / |m| < 2^(a-14) / |m|; a quotient
+// that is a half-integer is representable and comes out exactly, so rint
+// takes the even side.  The quotient stays within 32767 in magnitude for any
+// m > 0, however small.
+__device__ __forceinline__ int code_i16(float x, double m)
+{
+    return (int)__builtin_rint((32767.0 * (double)x) / m);
+}
+
+// INT16 codes q = Round(32767 x / m), m = max|X| read from *maxabs (m = 0
+// gives all-zero codes).  HBM-bound: the FP64 division per element hides
+// behind the 6 bytes each element moves.
 __global__ void __launch_bounds__(kThreads)
 quantize_kernel(const float *__restrict__ x, int64_t n, int16_t *__restrict__ q,
                 const float *__restrict__ maxabs)
 {
-    const float m = *maxabs;
-    const float inv = m > 0.0f ? 32767.0f / m : 0.0f;
+    const float mf = *maxabs;
+    const bool zero = !(mf > 0.0f);
+    const double m = zero ? 1.0 : (double)mf;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     const int64_t t0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     int64_t done = 0;
@@ -192,15 +207,16 @@ quantize_kernel(const float *__restrict__ x, int64_t n, int16_t *__restrict__ q,
             u32x4 o;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const int c0 = (int)__builtin_rintf(v[2 * t] * inv);
-                const int c1 = (int)__builtin_rintf(v[2 * t + 1] * inv);
+                const int c0 = zero ? 0 : code_i16(v[2 * t], m);
+                const int c1 = zero ? 0 : code_i16(v[2 * t + 1], m);
                 o[t] = ((uint32_t)c0 & 0xffffu) | ((uint32_t)c1 << 16);
             }
             __builtin_nontemporal_store(o, q4 + i);
         }
         done = n8 * 8;
     }
-    for (int64_t i = done + t0; i < n; i += stride) q[i] = (int16_t)(int)__builtin_rintf(x[i] * inv);
+    for (int64_t i = done + t0; i < n; i += stride)
+        q[i] = (int16_t)(zero ? 0 : code_i16(x[i], m));
 }
 
 }  // namespace

@@ -20,3 +20,14 @@ def pytest_configure(config):
 def orc():
     from oracle import oracle
     return oracle.default()
+
+
+@pytest.fixture(scope="session", autouse=True)
+def built_library_matches_sources():
+    """Every session that finds libheal.so checks that it was built from the
+    sources in this tree, so that a stale binary cannot pass for the code."""
+    from paper_2606_21023_amd import build as hbuild
+    if os.path.exists(hbuild.LIBRARY):
+        import paper_2606_21023_amd as heal
+        heal.check_build()
+    yield

@@ -16,8 +16,9 @@ The FP16 forms (HEAL-Base, HEAL-Full) and the INT16 score product (HEAL+)
 have pins of the same kinds: binary16 rounding against numpy's float16 casts,
 hand-derived golden pairs, the defining property of the weight exponent,
 closed-form error bounds against exact rational products, integer inputs, the
-exact identity hi + lo/2^10 = q of the INT16 unpack, and the paper's INT16
-error and MSE bounds.
+exact identity hi + lo/2^10 = q of the INT16 unpack, INT16 codes against the
+exact rational rounding (golden workload elements and values next to ties),
+and the paper's INT16 error and MSE bounds.
 
 The mutation tests run the same pins against oracles with planted mistakes.
 """
@@ -624,32 +625,98 @@ def pin_gemm_f16w_rows(orc, seed=12):
 # INT16 codes and dual-FP16 scores (HEAL+)
 # --------------------------------------------------------------------------
 
+def exact_i16_code(x, m):
+    """Round(32767 x / m) of the real quotient, ties to even (exact rationals)."""
+    if float(m) == 0.0:
+        return 0
+    return round(Fraction(32767) * Fraction(float(x)) / Fraction(float(m)))
+
+
+def load_quantize_golden():
+    rows = []
+    with open(os.path.join(GOLDEN, "quantize_i16_cases.txt")) as f:
+        for line in f:
+            line = line.split("#")[0].strip()
+            if line:
+                xb, mb, q = line.split()
+                rows.append((int(xb, 16), int(mb, 16), int(q)))
+    return rows
+
+
+def pin_quantize_i16_golden(orc):
+    """Elements of the attention workload whose exactly rounded code differs
+    from an FP32 decision (tests/golden/quantize_i16_cases.txt, derived in
+    exact rationals): each is quantized together with an element equal to its
+    tensor's maximum, so max|X| is the recorded m."""
+    rows = load_quantize_golden()
+    assert len(rows) >= 40
+    for xb, mb, code in rows:
+        x, m = _f32_from_bits(np.uint32(xb)), _f32_from_bits(np.uint32(mb))
+        assert exact_i16_code(x, m) == code, "golden file entry 0x%08x is not Round" % xb
+        q, mq = orc.quantize_i16(np.array([x, m, -x], np.float32))
+        assert mq == m, "max|X| of the golden case"
+        assert (int(q[0]), int(q[1]), int(q[2])) == (code, 32767, -code), \
+            "golden x=0x%08x m=0x%08x: code %d, expected %d" % (xb, mb, int(q[0]), code)
+
+
+def near_half_integer_inputs(rng, m, count):
+    """FP32 x whose quotient 32767 x / m lies within a few ulps of a
+    half-integer n + 1/2: the nearest float to (n + 1/2) m / 32767 and its two
+    neighbours, for random n of both signs."""
+    n = rng.integers(-32767, 32767, size=count)
+    c = ((n + 0.5) * float(m) / 32767.0).astype(np.float32)
+    xs = np.concatenate([c, np.nextafter(c, np.float32(np.inf)), np.nextafter(c, np.float32(-np.inf))])
+    return xs[np.abs(xs) <= m]
+
+
 def pin_quantize_i16(orc, seed=13):
-    """INT16 codes: golden values, the range, the extremes, all-zero input, and
-    the paper's INT16 error bound |x - q*D| <= D/2 (D = max|X| / 32767), here
-    with the slack of the two FP32 roundings of the decision."""
+    """INT16 codes by the definition Round(32767 x / max|X|) (Section 4, Q/K/V
+    paragraph): golden ties, the range, the extremes, all-zero input, codes
+    equal to the exact rational rounding on random values and on values whose
+    quotient sits next to a half-integer, tiny and subnormal maxima, and the
+    paper's INT16 error bound |x - q D| <= D/2 (D = max|X| / 32767) with no
+    slack."""
     x = np.array([2.0, -1.0, 0.5, 1e-30, 0.0, -2.0, 1.5], np.float32)
     q, m = orc.quantize_i16(x)
-    # inv = 32767/2 = 16383.5 exactly; -1 -> -16383.5, a tie, to even -16384;
-    # 0.5 -> 8191.75 -> 8192; 1.5 -> 24575.25 -> 24575
+    # 32767 x / 2: -1 -> -16383.5, a tie, to even -16384; 0.5 -> 8191.75 -> 8192;
+    # 1.5 -> 24575.25 -> 24575
     assert m == 2.0 and list(q) == [32767, -16384, 8192, 0, 0, -32767, 24575], (list(q), m)
-    # max|X| = 32767 gives inv = 1 exactly, so t = x and halves are ties to even
+    # max|X| = 32767: the quotient is x itself, halves are ties to even
     q, m = orc.quantize_i16(np.array([32767.0, 2.5, -3.5, 0.5, 1.5, -0.5, 7.25], np.float32))
     assert m == 32767.0 and list(q) == [32767, 2, -4, 0, 2, 0, 7], (list(q), m)
+    # max|X| = 3 (not a divisor of 32767): 32767 * 1 / 3 = 10922.33 -> 10922,
+    # 32767 * 2.25 / 3 = 24575.25 -> 24575, 32767 * (-1.5) / 3 = -16383.5 -> -16384
+    q, m = orc.quantize_i16(np.array([3.0, 1.0, 2.25, -1.5], np.float32))
+    assert m == 3.0 and list(q) == [32767, 10922, 24575, -16384], (list(q), m)
     q0, m0 = orc.quantize_i16(np.zeros(9, np.float32))
     assert m0 == 0.0 and np.all(q0 == 0), "all-zero tensor"
     rng = np.random.default_rng(seed)
-    for scale in (1e-3, 1.0, 300.0):
+    cases = []
+    for scale in (1e-3, 1.0, 300.0, 1e-36):
         x = (rng.standard_normal(50000) * scale).astype(np.float32)
         x[17] = np.float32(-40.0 * scale)  # an outlier sets max|X|
+        cases.append((x, np.float32(40.0 * scale), 17))
+        m = np.float32(40.0 * scale)
+        near = near_half_integer_inputs(rng, m, 3000)
+        cases.append((np.concatenate([np.array([m], np.float32), near]), m, 0))
+    # subnormal maxima: the smallest subnormal and a few steps of it
+    tiny = np.array([2.0 ** -149, -2.0 ** -149, 0.0], np.float32)
+    cases.append((tiny, np.float32(2.0 ** -149), 0))
+    sub = (rng.integers(-1000, 1001, size=2000) * 2.0 ** -149).astype(np.float32)
+    sub[0] = np.float32(1000 * 2.0 ** -149)
+    cases.append((sub, np.float32(1000 * 2.0 ** -149), 0))
+    for x, mexp, imax in cases:
         q, m = orc.quantize_i16(x)
-        assert m == np.float32(40.0 * scale)
-        assert q.min() >= -32767 and q.max() <= 32767 and q[17] == -32767
+        assert m == mexp, "max|X| %r, expected %r" % (m, mexp)
+        assert q.min() >= -32767 and q.max() <= 32767
+        assert abs(int(q[imax])) == 32767, "the maximum's code"
         D = Fraction(float(m)) / 32767
-        worst = Fraction(0)
-        for i in rng.choice(x.size, 400, replace=False):
-            worst = max(worst, abs(Fraction(float(x[i])) - q[i] * D))
-        assert worst <= D / 2 * (1 + Fraction(1, 2 ** 7)), "INT16 error exceeds D/2"
+        sample = np.arange(x.size) if x.size <= 4000 else rng.choice(x.size, 4000, replace=False)
+        for i in sample:
+            want = exact_i16_code(x[i], m)
+            assert int(q[i]) == want, "x=%r m=%r: code %d, exact Round %d" % (
+                float(x[i]), float(m), int(q[i]), want)
+            assert abs(Fraction(float(x[i])) - int(q[i]) * D) <= D / 2, "INT16 error exceeds D/2"
 
 
 def pin_int16_mse_ratio(orc, seed=14):
@@ -681,21 +748,32 @@ def pin_unpack_i16_exhaustive(orc):
 
 def pin_scores_i16(orc, seed=15):
     """The four dual-FP16 products sum to the exact integer dot product of the
-    codes (closed form), and C rounds factor * S once, with
-    factor = (maxQ/32767) (maxK/32767) alpha up to three FP32 roundings."""
+    codes (closed form); the factor is the dequantisation of both codes times
+    alpha, alpha (maxQ / 32767)(maxK / 32767), within 2^-51 of its exact value;
+    C is the FP32 rounding of factor * S (exact rationals)."""
     rng = np.random.default_rng(seed)
     M, N, K = 9, 7, 64
     Q = rng.integers(-32767, 32768, size=(M, K)).astype(np.int16)
     Kt = rng.integers(-32767, 32768, size=(N, K)).astype(np.int16)
     Q[0, :] = 32767
     Kt[0, :] = -32767
-    mq, mk, alpha = np.float32(2.5), np.float32(0.75), np.float32(1.0 / np.sqrt(128.0))
-    C, S = orc.scores_i16(Q, Kt, mq, mk, alpha)
-    exact = Q.astype(np.int64) @ Kt.astype(np.int64).T
-    assert np.array_equal(S, exact.astype(np.float64)), "scores: S != integer dot product"
-    f = (float(mq) / 32767.0) * (float(mk) / 32767.0) * float(alpha)
-    ref = f * exact.astype(np.float64)
-    assert np.all(np.abs(C - ref) <= np.abs(ref) * 2.0 ** -21), "scores: C != factor * S"
+    for mq, mk, alpha in ((2.5, 0.75, 1.0 / np.sqrt(128.0)), (5.0978498, 5.571465, 0.125),
+                          (1e-20, 3e-19, 0.7)):
+        mq, mk, alpha = np.float32(mq), np.float32(mk), np.float32(alpha)
+        C, S = orc.scores_i16(Q, Kt, mq, mk, alpha)
+        exact = Q.astype(np.int64) @ Kt.astype(np.int64).T
+        assert np.array_equal(S, exact.astype(np.float64)), "scores: S != integer dot product"
+        f = orc.scores_factor(mq, mk, alpha)
+        fx = Fraction(float(alpha)) * Fraction(float(mq)) * Fraction(float(mk)) / 32767 ** 2
+        assert abs(Fraction(f) - fx) <= fx * Fraction(1, 2 ** 51), "scores factor"
+        for i in range(M):
+            for j in range(N):
+                v = fx * int(exact[i, j])
+                err = abs(Fraction(float(C[i, j])) - v)
+                # half an FP32 step: 2^-24 |v| for normal results, 2^-150 below 2^-126
+                half_step = max(abs(v) * Fraction(1, 2 ** 24), Fraction(1, 2 ** 150))
+                assert err <= half_step * (1 + Fraction(1, 2 ** 20)), \
+                    "scores: C != f32(factor * S) at (%d, %d)" % (i, j)
     rows = np.array([8, 0, 3])
     Cr, Sr = orc.scores_i16(Q, Kt, mq, mk, alpha, rows=rows)
     assert np.array_equal(Cr, C[rows]) and np.array_equal(Sr, S[rows]), "row subset differs"
@@ -707,4 +785,5 @@ SMALL_PINS = [pin_golden_split, pin_split_vs_library, pin_split_properties, pin_
               pin_f16_rne_vs_library, pin_golden_split_f16, pin_split_f16_vs_library,
               pin_split_f16_properties, pin_weight_exponent, pin_f16_weights_vs_library,
               pin_gemm_f16w_integer, pin_gemm_f16w_bruteforce, pin_gemm_f16w_rows,
-              pin_quantize_i16, pin_int16_mse_ratio, pin_unpack_i16_exhaustive, pin_scores_i16]
+              pin_quantize_i16, pin_quantize_i16_golden, pin_int16_mse_ratio,
+              pin_unpack_i16_exhaustive, pin_scores_i16]

@@ -41,6 +41,16 @@ def test_status_strings_and_version():
     assert L.heal_version() >= 100
 
 
+def test_build_id_matches_the_sources():
+    """The library reports the hash of the sources it was built from, and it
+    is the hash of the sources in this tree; an edit of any source changes it."""
+    from paper_2606_21023_amd import build as hbuild
+    got = heal.build_id()
+    assert re.fullmatch(r"[0-9a-f]{16}", got), got
+    assert got == hbuild.source_hash()
+    assert heal.check_build() == got
+
+
 def test_select_instance_depends_on_m_and_n_only():
     assert heal.select_instance(1, 4096) == heal.INSTANCE_SKINNY
     assert heal.select_instance(64, 128256) == heal.INSTANCE_SKINNY

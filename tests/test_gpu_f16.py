@@ -404,6 +404,41 @@ def test_quantize_bitwise(orc, n, offset):
     assert np.array_equal(qd.cpu().numpy(), qo), "INT16 codes differ"
 
 
+def test_quantize_golden_near_ties(orc):
+    """Elements of the attention workload whose exactly rounded code differs
+    from an FP32 decision (tests/golden/quantize_i16_cases.txt, exact rational
+    codes): the GPU code is the golden one."""
+    import pins
+    for xb, mb, code in pins.load_quantize_golden():
+        x = np.array([xb, mb, xb ^ 0x80000000], np.uint32).view(np.float32)
+        announce("quantize golden x=0x%08x m=0x%08x" % (xb, mb))
+        q, m = heal.heal_quantize_i16(to_dev(x))
+        torch.cuda.synchronize()
+        assert m.item() == float(x[1])
+        assert q.cpu().numpy().tolist() == [code, 32767, -code], "x=0x%08x" % xb
+
+
+@pytest.mark.parametrize("m", [40.0, 5.0978498, 1e-3, 4e-35, 1e-36, 2.0 ** -140],
+                         ids=lambda v: "%g" % v)
+def test_quantize_next_to_ties_and_tiny_maxima(orc, m):
+    """Values whose quotient 32767 x / m lies within an ulp of a half-integer,
+    for ordinary, tiny (32767 / m overflows FP32) and subnormal maxima: codes
+    bitwise equal to the oracle's exact rounding."""
+    import pins
+    rng = np.random.default_rng(int(abs(np.log2(m))) + 3)
+    m32 = np.float32(m)
+    x = np.concatenate([np.array([m32, -m32], np.float32),
+                        pins.near_half_integer_inputs(rng, m32, 20000),
+                        np.clip(rng.standard_normal(5000).astype(np.float32) * (m32 / 4),
+                                -m32, m32)])
+    announce("quantize next to ties, m=%g n=%d" % (m, x.size))
+    qd, md = heal.heal_quantize_i16(to_dev(x))
+    torch.cuda.synchronize()
+    qo, mo = orc.quantize_i16(x)
+    assert md.item() == float(mo) == float(m32)
+    assert np.array_equal(qd.cpu().numpy(), qo), "INT16 codes differ"
+
+
 def test_quantize_all_zero():
     announce("quantize all-zero")
     q, m = heal.heal_quantize_i16(torch.zeros(1000, device="cuda"))
@@ -422,9 +457,9 @@ def scores_absprod(Q, Kt, f):
     return abs(f) * (np.abs(Q.astype(np.float64)) @ np.abs(Kt.astype(np.float64)).T)
 
 
-def factor(mq, mk, alpha):
-    return float(np.float32(np.float32(np.float32(mq) / np.float32(32767)) *
-                            np.float32(np.float32(mk) / np.float32(32767))) * np.float32(alpha))
+def factor(orc, mq, mk, alpha):
+    """The oracle's FP64 dequantisation factor alpha (mq/32767)(mk/32767)."""
+    return orc.scores_factor(mq, mk, alpha)
 
 
 SCORE_SHAPES = [(1, 1, 1, 1), (1, 17, 31, 33), (2, 64, 70, 128), (3, 129, 257, 64),
@@ -442,7 +477,7 @@ def test_scores_parity(orc, shape):
                              torch.tensor([mk], device="cuda"), alpha)
     torch.cuda.synchronize()
     S = S.cpu().numpy()
-    f = factor(mq, mk, alpha)
+    f = factor(orc, mq, mk, alpha)
     for b in range(bat):
         _, So = orc.scores_i16(Q[b], Kt[b], mq, mk, alpha)
         check_tolerance(S[b], f * So, scores_absprod(Q[b], Kt[b], f), "scores %s b%d" % (shape, b))
@@ -479,7 +514,7 @@ def test_scores_attention_workload(orc):
     announce("scores workload: scores")
     S = heal.heal_scores_i16(q, k, mq, mk, w.alpha)
     torch.cuda.synchronize()
-    f = factor(mqo, mko, w.alpha)
+    f = factor(orc, mqo, mko, w.alpha)
     for h in (0, 17, 31):
         rows = _rows(w.M, 4, h)
         Sr = S[h][torch.from_numpy(rows).cuda()].cpu().numpy()
@@ -531,7 +566,7 @@ def test_scores_padded_rows(orc):
     S = heal.heal_scores_i16(Qv, Kv, torch.tensor([mq], device="cuda"),
                              torch.tensor([mk], device="cuda"), 0.5)
     torch.cuda.synchronize()
-    f = factor(mq, mk, 0.5)
+    f = factor(orc, mq, mk, 0.5)
     for b in range(bat):
         Q, Kt = np.ascontiguousarray(Qw[b, :, :K]), np.ascontiguousarray(Kw[b, :, :K])
         _, So = orc.scores_i16(Q, Kt, mq, mk, 0.5)

@@ -53,10 +53,11 @@ MUTATIONS = [
     ("output_scale_sign", "ldexp(s_hi + ldexp(s_lo, -10), -e)", "ldexp(s_hi + ldexp(s_lo, -10), e)"),
     ("full_residual_subtracted", "ldexp(s_hi + ldexp(s_lo, -10), -e)",
      "ldexp(s_hi - ldexp(s_lo, -10), -e)"),
-    ("quant_ties_away", "q[i] = (int16_t)rintf(t);", "q[i] = (int16_t)roundf(t);"),
-    ("quant_2^15", "float inv = m > 0.0f ? 32767.0f / m : 0.0f;",
-     "float inv = m > 0.0f ? 32768.0f / m : 0.0f;"),
-    ("quant_truncates", "q[i] = (int16_t)rintf(t);", "q[i] = (int16_t)t;"),
+    ("quant_ties_away", "q[i] = (int16_t)rint(t);", "q[i] = (int16_t)round(t);"),
+    ("quant_2^15", "(32767.0 * (double)x[i]) / (double)m", "(32768.0 * (double)x[i]) / (double)m"),
+    ("quant_truncates", "q[i] = (int16_t)rint(t);", "q[i] = (int16_t)t;"),
+    ("quant_fp32_decision", "(32767.0 * (double)x[i]) / (double)m", "x[i] * (32767.0f / m)"),
+    ("quant_fp32_quotient", "(32767.0 * (double)x[i]) / (double)m", "(float)(32767.0f * x[i] / m)"),
     ("unpack_lo_unshifted", "*lo = oracle_f16_rne(((double)q - oracle_f16_value(h)) * 1024.0);",
      "*lo = oracle_f16_rne(((double)q - oracle_f16_value(h)));"),
     ("scores_drop_lolo", "+ ql[k] * bh[k] + ql[k] * bl[k];", "+ ql[k] * bh[k];"),
@@ -65,7 +66,10 @@ MUTATIONS = [
      "int64_t i = r < M ? r : M - 1;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    split_f16_one("),
     ("scores_row_subset_ignored", "int64_t i = rows ? rows[r] : r;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    oracle_unpack_i16(Q",
      "int64_t i = r < M ? r : M - 1;\n                for (int64_t k = 0; k < K; ++k) {\n                    uint16_t h, l;\n                    oracle_unpack_i16(Q"),
-    ("scores_no_alpha", "float factor = prod * alpha;", "float factor = prod;"),
+    ("scores_no_alpha", "return (double)alpha * (double)maxQ", "return (double)maxQ"),
+    ("scores_factor_fp32",
+     "return (double)alpha * (double)maxQ * (double)maxK / (32767.0 * 32767.0);",
+     "return (double)(((maxQ / 32767.0f) * (maxK / 32767.0f)) * alpha);"),
 ]
 
 
