@@ -48,3 +48,59 @@ def test_source_hash_covers_each_kernel_family():
     assert all(len(h) == 16 for h in hashes.values())
     # each family hashes a different kernel source
     assert len(set(hashes.values())) == len(hashes)
+
+
+def _write_csv(path, header, rows):
+    import csv
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w", newline="") as f:
+        w = csv.writer(f, quoting=csv.QUOTE_NONNUMERIC)
+        w.writerow(header)
+        w.writerows(rows)
+
+
+def test_profile_summary_averages_the_timed_dispatches(tmp_path):
+    """--profile-summary on a synthetic rocprofv3 directory: the measured
+    kernel's dispatches are split into warm-up, timed and statistics-pass
+    launches by order, and the timed average and traffic come out right."""
+    W, K = 2, 3
+    name = "void heal::(anonymous namespace)::gemm_large8_kernel<false, false, false>(heal::GemmArgs)"
+    # warm-up launches 5 us, timed 2 us, statistics pass 3 us; another kernel in between
+    durs = [5000] * W + [2000] * K + [3000] * K
+    trace, t = [], 1000
+    for i, d in enumerate(durs):
+        trace.append(["KERNEL_DISPATCH", "Agent 1", 1, 0, 1, 2 * i + 1, 7, name, 1, t, t + d])
+        trace.append(["KERNEL_DISPATCH", "Agent 1", 1, 0, 1, 2 * i + 2, 8, "copy", 1, t + d,
+                      t + d + 10])
+        t += d + 100
+    d = str(tmp_path)
+    _write_csv(os.path.join(d, "trace", "run_kernel_trace.csv"),
+               ["Kind", "Agent_Id", "Queue_Id", "Stream_Id", "Thread_Id", "Dispatch_Id",
+                "Kernel_Id", "Kernel_Name", "Correlation_Id", "Start_Timestamp", "End_Timestamp"],
+               trace)
+    _write_csv(os.path.join(d, "trace", "run_kernel_stats.csv"),
+               ["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs"],
+               [[name, W + 2 * K, sum(durs), sum(durs) / len(durs), 99.0, 2000, 5000]])
+    cc = ["Correlation_Id", "Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    _write_csv(os.path.join(d, "p1", "run_counter_collection.csv"), cc,
+               [[1, 1, name, "FETCH_SIZE", 100.0]] +
+               [[2 + i, 2 + i, "__amd_rocclr_copyBuffer", "FETCH_SIZE", 524288.0] for i in range(3)])
+    _write_csv(os.path.join(d, "p2", "run_counter_collection.csv"), cc,
+               [[1, 1, name, "WRITE_SIZE", 50.0]] +
+               [[2 + i, 2 + i, "__amd_rocclr_copyBuffer", "WRITE_SIZE", 1048576.0] for i in range(3)])
+    line = {"warmup": W, "steps": K, "config": {"method": "bf16x3", "workload": "square8192",
+                                                "M": 8192, "N": 8192},
+            "roofline": {"kernel": "gemm_large8_kernel (256x256 tiles)", "avg_launch_us": 2.0,
+                         "achieved": 1000.0, "peak": 2000.0, "unit": "TFLOP/s", "bound": "mfma",
+                         "frac": 0.5, "per_launch": "x"}}
+    with open(os.path.join(d, "trace.log"), "w") as f:
+        f.write("noise\n" + json.dumps(line) + "\n")
+    with open(os.path.join(d, "commands.txt"), "w") as f:
+        f.write("rocprofv3 --kernel-trace --stats -- python3 bench.py\n")
+    text = bench.profile_summary(d)
+    assert "| rocprofv3, the timed dispatches | 3 | 2.00 | 2.00 | 2.00 |" in text
+    assert "| rocprofv3, the statistics pass | 3 | 3.00 |" in text
+    assert "| rocprofv3, warm-up dispatches | 2 | 5.00 |" in text
+    assert "timed dispatches' trace average: 0.5000" in text
+    # FETCH x2 (524288 KiB per 1 GiB copy), WRITE x1: 100 KiB * 2 + 50 KiB
+    assert "Traffic %.4g bytes" % (100 * 1024 * 2.0 + 50 * 1024) in text
