@@ -108,8 +108,9 @@ __device__ __forceinline__ u32x4 bload(__amdgpu_buffer_rsrc_t r, uint32_t voff)
 
 // R: register sets of staged operands.  R = 1: the next stage is loaded
 // while the current one is multiplied out (one stage of compute to hide the
-// load).  R = 2: a ring of two sets, each reloaded two stages ahead, for
-// narrow tiles whose compute per stage is too short to hide a load.
+// load).  R = 2, 4, ...: a ring of R sets, each reloaded R stages ahead, for
+// narrow tiles whose compute per stage is too short to hide a load (their
+// weight stream is bound by the bytes in flight per CU).
 template <int OP, int BM, int BN, int WM, int WN, int NT, int BK, int R, bool VEC>
 __global__ void __launch_bounds__(NT)
 gemm_op_kernel(OpArgs p)
@@ -128,8 +129,8 @@ gemm_op_kernel(OpArgs p)
     // the first CWAVES waves compute one wave tile each; all NT threads load
     // and convert (extra waves only help move a narrow tile's operands)
     constexpr int CWAVES = WAVES_M * (BN / WN);
-    static_assert(BK % 32 == 0 && BK <= 256, "stage depth");
-    static_assert(R == 1 || R == 2, "register sets");
+    static_assert(BK % 32 == 0 && BK <= 512, "stage depth");
+    static_assert(R >= 1 && R <= 8, "register sets");
     static_assert(BM % WM == 0 && BN % WN == 0 && WM % 16 == 0 && WN % 16 == 0, "wave tiling");
     static_assert(CWAVES * 64 <= NT && NT % 64 == 0, "compute waves exceed the workgroup");
 
@@ -426,28 +427,51 @@ gemm_op_kernel(OpArgs p)
                 if (kt + 1 < nk) step(smem1, smem0, kt + 1);
             }
         } else {
-            // stage t lives in register set t % 2; at step kt the set of
-            // stage kt+1 is stored and then reloaded with stage kt+3, so each
-            // load has two steps to arrive.  Reloads past the last stage are
-            // clamped to it (redundant loads whose data is never used).
+            // stage t lives in register set t % R; at step kt the set of
+            // stage kt+1 is stored and then reloaded with stage kt+1+R, so
+            // each load has R steps to arrive.  Reloads past the last stage
+            // are clamped to it (redundant loads whose data is never used).
+            // The loop is unrolled by R (R even) so that the register set of
+            // every step, and its LDS buffer, are compile-time constants.
+            static_assert(R % 2 == 0, "R >= 2 register sets come in pairs");
             const int64_t last = nk - 1;
             auto clamp = [&](int64_t t) { return (t < last ? t : last) * BK; };
             auto step = [&](const char *cur, char *nxt, int set, int64_t kt) {
-                if (computes) compute_stage(cur);
+                if (computes && kt < nk) compute_stage(cur);
                 store_stage(nxt, set);
-                load_stage(set, clamp(kt + 3));
+                load_stage(set, clamp(kt + 1 + R));
                 __syncthreads();
             };
             if (nk > 0) {
                 load_stage(0, 0);
                 store_stage(smem0, 0);
-                load_stage(1, clamp(1));
-                load_stage(0, clamp(2));
+                // the sets are issued in ring order (scheduling barriers keep
+                // the compiler from interleaving them), the order the loop
+                // keeps, so that every wait before a store is exact
+#pragma unroll
+                for (int t = 1; t < R; ++t) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    load_stage(t, clamp(t));
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                load_stage(0, clamp(R));
+                __builtin_amdgcn_sched_barrier(0);
                 __syncthreads();
             }
-            for (int64_t kt = 0; kt < nk; kt += 2) {
-                step(smem0, smem1, 1, kt);
-                if (kt + 1 < nk) step(smem1, smem0, 0, kt + 1);
+            // Every group of R steps runs whole, loads and stores included;
+            // only the multiply of a step past the last stage is skipped (at
+            // most R - 1 steps that load and store clamped copies).  With a
+            // step under a branch the compiler has to assume a path around
+            // it and waits for every outstanding load before each store
+            // (vmcnt(0)), which empties the ring.
+            for (int64_t kt0 = 0; kt0 < nk; kt0 += R) {
+#pragma unroll
+                for (int u = 0; u < R; ++u) {
+                    if (u & 1)
+                        step(smem1, smem0, (u + 1) % R, kt0 + u);
+                    else
+                        step(smem0, smem1, (u + 1) % R, kt0 + u);
+                }
             }
         }
 
@@ -828,6 +852,292 @@ hipError_t launch_op8(const OpArgs &a, hipStream_t stream)
 // 16-byte units along K, and every byte offset inside a tile below 2^31.
 // (Packed B is always read with buffer loads; the caller bounds K so that a
 // tile's packed offsets stay below 2^31.)
+// ---------------------------------------------------------------------------
+// Streamed narrow tiles of the packed-B products (M <= 64, one 16-column
+// block of the packed operand per workgroup).
+//
+// A K-sum of an output element stays in one wave (the fixed order), so a
+// narrow tile is one chain of dependent MFMAs per 16-row block, K/32 x
+// products long.  With one workgroup barrier per stage, every stage of that
+// chain also waits for the fragment reads of its first chunk and for the
+// barrier.  Here the roles are split: LW loader waves move A (converting it)
+// and the packed B block into a ring of D LDS stages, one compute wave walks
+// the ring chunk by chunk, reading the next chunk's fragments while the
+// current chunk's MFMAs run, and the two sides hand stages over through LDS
+// counters instead of barriers:
+//   ready[s]  the loader waves that have stored the stage now in ring slot s
+//             (a stage t in slot t % D is complete when ready reaches
+//             (t / D + 1) * LW);
+//   consumed  the stages the compute wave has finished reading (a loader
+//             stores stage t only once consumed >= t - D + 1).
+// A loader makes its LDS stores complete (s_waitcnt lgkmcnt(0)) before it
+// adds to ready, and a wave's LDS requests are served in order, so a
+// consumer that has seen the count reads the stored data.  Every wait on a
+// counter polls at most HEAL_STREAM_SPIN_LIMIT times (seconds, far beyond any
+// real wait): a defect that stalled a counter would give a wrong result
+// instead of a kernel that never ends.
+// Same conversions, MFMAs, chunk order and product order as gemm_op_kernel,
+// so the bits are those of every other instance.
+#ifndef HEAL_STREAM_SPIN_LIMIT
+#define HEAL_STREAM_SPIN_LIMIT (1 << 20)
+#endif
+
+__device__ __forceinline__ uint32_t lds_load_relaxed(const uint32_t *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ void spin_until_at_least(const uint32_t *p, uint32_t target)
+{
+    for (int i = 0; i < HEAL_STREAM_SPIN_LIMIT; ++i) {
+        if (lds_load_relaxed(p) >= target) return;
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+template <int OP, int BM, int BK, int D, int LW, int PF, int R>
+__global__ void __launch_bounds__((LW + 1) * 64)
+gemm_op_stream_kernel(OpArgs p)
+{
+    using O = OpT<OP>;
+    static_assert(!O::A_I16 && !O::B_ROWS, "packed-B products of an FP32 A");
+    constexpr int ROWB = BK * 2;                 // bytes per LDS row of one A plane
+    constexpr int NCH = BK / 8;
+    constexpr int RPW = BK >= 64 ? 1 : 64 / BK;
+    constexpr int SWM = (NCH < 8 ? NCH : 8) - 1;
+    constexpr int KS = BK / 32;                  // MFMA chunks per stage
+    constexpr int FM = BM / 16;
+    constexpr int A_PLANE = BM * ROWB;
+    constexpr int B_PLANE = KS * 1024;           // one packed 16-column block, one plane
+    constexpr int STAGE = O::AP * A_PLANE + O::BP * B_PLANE;
+    constexpr int NL = LW * 64;                  // loader threads
+    constexpr int A_UPR = BK / 4;                // 16-byte units per A row
+    constexpr int A_UNITS = BM * A_UPR;
+    constexpr int A_IT = (A_UNITS + NL - 1) / NL;
+    constexpr int B_UNITS = KS * O::BP * 64;
+    constexpr int B_IT = (B_UNITS + NL - 1) / NL;
+    static_assert(BK % 32 == 0 && BK <= 512 && BM % 16 == 0 && BM <= 64, "tile");
+    static_assert(D >= 2 && D * STAGE <= 159 * 1024, "the LDS ring must fit one CU");
+
+    __shared__ __attribute__((aligned(16))) char ring[D * STAGE];
+    __shared__ uint32_t ready[D];
+    __shared__ uint32_t consumed;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int fr = lane & 15;
+    const int fg = lane >> 4;
+
+    auto swz = [](int row) { return (row / RPW) & SWM; };
+    auto chunk_off = [&](int row, int c) { return row * ROWB + ((c ^ swz(row)) << 4); };
+    auto quad_off = [&](int row, int kq) {
+        return row * ROWB + (((kq >> 1) ^ swz(row)) << 4) + ((kq & 1) << 3);
+    };
+
+    // one 16-column block per workgroup, XCD-aware numbering
+    const int64_t nb = (int64_t)gridDim.x;
+    int64_t bid = blockIdx.x;
+    {
+        const int64_t x = bid & 7, i = bid >> 3, q = nb >> 3, r = nb & 7;
+        bid = x * q + (x < r ? x : r) + i;
+    }
+    const int64_t n0 = bid * 16;
+    const int64_t M = p.M, N = p.N, K = p.K;
+    const int64_t nk = (K + BK - 1) / BK;
+    const int64_t KC = (K + 31) / 32;
+
+    if (tid < D) ready[tid] = 0u;
+    if (tid == 0) consumed = 0u;
+    __syncthreads();
+    if (nk == 0) return;
+
+    const char *Ab = reinterpret_cast<const char *>(p.A);
+    const char *Bb = reinterpret_cast<const char *>(p.B);
+    const __amdgpu_buffer_rsrc_t rsrc_a = make_rsrc(Ab);
+    const __amdgpu_buffer_rsrc_t rsrc_b = make_rsrc(Bb + (n0 / 16) * KC * O::BP * 1024);
+
+    if (wave < LW) {
+        // ---------------- loader waves ----------------
+        u32x4 ra[R][A_IT], rb[R][B_IT];
+        const int64_t last = nk - 1;
+        auto load_stage = [&](int set, int64_t t) {
+            const int64_t k0 = (t < last ? t : last) * BK;
+#pragma unroll
+            for (int it = 0; it < A_IT; ++it) {
+                const int u = it * NL + tid;
+                if (A_UNITS % NL != 0 && u >= A_UNITS) continue;
+                const int row = u / A_UPR, c = u % A_UPR;
+                const int64_t k = k0 + (int64_t)c * 4;
+                const bool ok = row < M && k < K;
+                ra[set][it] = bload(rsrc_a, ok ? (uint32_t)(((int64_t)row * p.lda + k) * 4) : kOOB);
+            }
+#pragma unroll
+            for (int it = 0; it < B_IT; ++it) {
+                const int u = it * NL + tid;
+                if (B_UNITS % NL != 0 && u >= B_UNITS) continue;
+                const int64_t kc = k0 / 32 + u / (O::BP * 64);
+                const bool ok = kc < KC;
+                rb[set][it] =
+                    bload(rsrc_b, ok ? (uint32_t)(((k0 / 32) * O::BP * 64 + u) * 16) : kOOB);
+            }
+        };
+        auto store_stage = [&](char *s, int set) {
+            char *a0 = s, *a1 = s + A_PLANE, *b0 = s + O::AP * A_PLANE;
+#pragma unroll
+            for (int it = 0; it < A_IT; ++it) {
+                const int u = it * NL + tid;
+                if (A_UNITS % NL != 0 && u >= A_UNITS) continue;
+                const int row = u / A_UPR, c = u % A_UPR;
+                const f32x4 xf = __builtin_bit_cast(f32x4, ra[set][it]);
+                const int off = quad_off(row, c);
+                if constexpr (OP == OP_BASE) {
+                    const u32x2 h = {cvt2_f16(xf.x, xf.y), cvt2_f16(xf.z, xf.w)};
+                    *reinterpret_cast<u32x2 *>(a0 + off) = h;
+                } else {
+                    uint32_t h0, l0, h1, l1;
+                    if constexpr (OP == OP_FULL) {
+                        split2_f16(xf.x, xf.y, h0, l0);
+                        split2_f16(xf.z, xf.w, h1, l1);
+                    } else {
+                        split2(xf.x, xf.y, h0, l0);
+                        split2(xf.z, xf.w, h1, l1);
+                    }
+                    const u32x2 h = {h0, h1}, l = {l0, l1};
+                    *reinterpret_cast<u32x2 *>(a0 + off) = h;
+                    *reinterpret_cast<u32x2 *>(a1 + off) = l;
+                }
+            }
+#pragma unroll
+            for (int it = 0; it < B_IT; ++it) {
+                const int u = it * NL + tid;
+                if (B_UNITS % NL != 0 && u >= B_UNITS) continue;
+                *reinterpret_cast<u32x4 *>(b0 + u * 16) = rb[set][it];
+            }
+        };
+        // stage t sits in register set t % R and is reloaded with stage t + R
+        // once stored (R stages of loads in flight per loader); every group
+        // of R steps runs whole (loads included), so that each wait before a
+        // store is for that set's loads alone
+        auto step = [&](int set, int64_t t) {
+            if (t < nk) {
+                if (t >= D) spin_until_at_least(&consumed, (uint32_t)(t - D + 1));
+                store_stage(ring + (t % D) * STAGE, set);
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                if (lane == 0)
+                    __hip_atomic_fetch_add(&ready[t % D], 1u, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+            load_stage(set, t + R);
+        };
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            load_stage(r, r);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        for (int64_t t = 0; t < nk; t += R) {
+#pragma unroll
+            for (int r = 0; r < R; ++r) step(r, t + r);
+        }
+        return;
+    }
+
+    // ---------------- the compute wave ----------------
+    f32x4 acc[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) acc[i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    // fragments of PF + 1 chunks: chunk k sits in buffer k % (PF + 1)
+    constexpr int NBUF = PF + 1;
+    static_assert(KS % NBUF == 0, "a stage holds whole turns of the fragment ring");
+    u32x4 fa[NBUF][FM], fl[NBUF][FM], fb[NBUF], fbl[NBUF];
+    auto read_chunk = [&](int buf, int64_t t, int ks) {
+        const char *s = ring + (t % D) * STAGE;
+        const char *a0 = s, *a1 = s + A_PLANE, *b0 = s + O::AP * A_PLANE;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int off = chunk_off(i * 16 + fr, ks * 4 + fg);
+            fa[buf][i] = *reinterpret_cast<const u32x4 *>(a0 + off);
+            if (O::AP == 2) fl[buf][i] = *reinterpret_cast<const u32x4 *>(a1 + off);
+        }
+        const int off = ks * O::BP * 1024 + lane * 16;
+        fb[buf] = *reinterpret_cast<const u32x4 *>(b0 + off);
+        if (O::BP == 2) fbl[buf] = *reinterpret_cast<const u32x4 *>(b0 + off + 1024);
+    };
+    auto mma_chunk = [&](int buf) {
+        const u32x4 bh = fb[buf];
+        u32x4 bs;
+        if constexpr (OP == OP_FULL)
+            bs = __builtin_bit_cast(u32x4, __builtin_bit_cast(f16x8, bh) * (_Float16)0x1p-10f);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            if constexpr (OP == OP_BASE) {
+                acc[i] = mma<false>(bh, fa[buf][i], acc[i]);
+            } else if constexpr (OP == OP_FULL) {
+                acc[i] = mma<false>(bh, fa[buf][i], acc[i]);
+                acc[i] = mma<false>(bs, fl[buf][i], acc[i]);
+            } else {
+                acc[i] = mma<true>(bh, fa[buf][i], acc[i]);
+                acc[i] = mma<true>(fbl[buf], fa[buf][i], acc[i]);
+                acc[i] = mma<true>(bh, fl[buf][i], acc[i]);
+            }
+        }
+    };
+    // Chunk k + PF is read while chunk k is multiplied out (a stage's
+    // MFMAs are too short to cover an LDS read one chunk ahead); the first
+    // read from stage t + 1 waits for that stage.  For the last stage the
+    // reads ahead go to its own chunks again, complete and still in their
+    // slot, so that no read sits under a branch and the wait before each
+    // chunk's MFMAs is for that chunk's reads alone.  The stage goes back to
+    // the loaders once the MFMAs of its last chunk have their operands;
+    // every lane writes the same count.
+    spin_until_at_least(&ready[0], (uint32_t)LW);
+#pragma unroll
+    for (int k = 0; k < PF; ++k) read_chunk(k, 0, k);
+    for (int64_t t = 0; t < nk; ++t) {
+        const int64_t tn = t + 1 < nk ? t + 1 : t;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int kk = ks + PF;
+            if (kk < KS) {
+                read_chunk(kk % NBUF, t, kk);
+            } else {
+                if (kk == KS)
+                    spin_until_at_least(&ready[tn % D], (uint32_t)((tn / D + 1) * LW));
+                read_chunk(kk % NBUF, tn, kk - KS);
+            }
+            mma_chunk(ks % NBUF);
+        }
+        __hip_atomic_store(&consumed, (uint32_t)(t + 1), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+
+    float *__restrict__ C = p.C;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int64_t m = i * 16 + fr;
+        const int64_t n = n0 + 4 * fg;
+        f32x4 v;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            if constexpr (OP == OP_BASE || OP == OP_FULL)
+                v[t] = ldexpf(acc[i][t], -p.e);
+            else
+                v[t] = acc[i][t];
+        }
+        if (m < M && n < N) {
+            float *cp = C + m * p.ldc + n;
+            if (p.vecC && n + 4 <= N) {
+                __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(cp));
+            } else {
+                cp[0] = v.x;
+                if (n + 1 < N) cp[1] = v.y;
+                if (n + 2 < N) cp[2] = v.z;
+                if (n + 3 < N) cp[3] = v.w;
+            }
+        }
+    }
+}
+
 template <int OP, int BM, int BN, int BK>
 bool vec_path_applies(const OpArgs &a)
 {
@@ -842,6 +1152,62 @@ bool vec_path_applies(const OpArgs &a)
         if (((int64_t)(BN - 1) * a.ldb + a.K + BK) * 2 >= lim) return false;
     }
     return true;
+}
+
+// The streamed narrow tiles: LDS ring depth, and per tile height the loader
+// waves and their register sets (stages of loads in flight per loader).
+#ifndef HEAL_OP_STREAM
+#define HEAL_OP_STREAM 1
+#endif
+#ifndef HEAL_STREAM_D
+#define HEAL_STREAM_D 4
+#endif
+#ifndef HEAL_STREAM16_LW
+#define HEAL_STREAM16_LW 4
+#endif
+#ifndef HEAL_STREAM16_R
+#define HEAL_STREAM16_R 2
+#endif
+#ifndef HEAL_STREAM32_LW
+#define HEAL_STREAM32_LW 8
+#endif
+#ifndef HEAL_STREAM32_R
+#define HEAL_STREAM32_R 4
+#endif
+#ifndef HEAL_STREAM64_LW
+#define HEAL_STREAM64_LW 8
+#endif
+#ifndef HEAL_STREAM64_R
+#define HEAL_STREAM64_R 4
+#endif
+#ifndef HEAL_STREAM16_BK
+#define HEAL_STREAM16_BK 256
+#endif
+#ifndef HEAL_STREAM32_BK
+#define HEAL_STREAM32_BK 128
+#endif
+#ifndef HEAL_STREAM64_BK
+#define HEAL_STREAM64_BK 64
+#endif
+// chunks read ahead by the compute wave
+#ifndef HEAL_STREAM16_PF
+#define HEAL_STREAM16_PF 3
+#endif
+#ifndef HEAL_STREAM32_PF
+#define HEAL_STREAM32_PF 3
+#endif
+#ifndef HEAL_STREAM64_PF
+#define HEAL_STREAM64_PF 1
+#endif
+
+template <int OP, int BM, int BK, int PF, int LW, int R>
+hipError_t launch_stream(const OpArgs &a, hipStream_t stream)
+{
+    const int64_t blocks = (a.N + 15) / 16;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((gemm_op_stream_kernel<OP, BM, BK, HEAL_STREAM_D, LW, PF, R>),
+                       dim3((unsigned)blocks), dim3((LW + 1) * 64), 0, stream, a);
+    return hipGetLastError();
 }
 
 template <int OP, int BM, int BN, int WM, int WN, int NT, int BK, int R = 1>
@@ -989,6 +1355,19 @@ hipError_t launch_op(int instance, const OpArgs &a, hipStream_t stream)
     case HEAL_INSTANCE_MEDIUM: return launch_cfg<OP, HEAL_OP_MEDIUM_CFG>(a, stream);
     case HEAL_INSTANCE_SKINNY: {
         const bool wide = (a.N + 255) / 256 >= HEAL_OP_WIDE_MIN_TILES;
+        if constexpr (OP != OP_SCORES) {
+            if (!wide && HEAL_OP_STREAM) {
+                if (a.M <= 16 && vec_path_applies<OP, 16, 16, HEAL_STREAM16_BK>(a))
+                    return launch_stream<OP, 16, HEAL_STREAM16_BK, HEAL_STREAM16_PF, HEAL_STREAM16_LW,
+                                         HEAL_STREAM16_R>(a, stream);
+                if (a.M > 16 && a.M <= 32 && vec_path_applies<OP, 32, 16, HEAL_STREAM32_BK>(a))
+                    return launch_stream<OP, 32, HEAL_STREAM32_BK, HEAL_STREAM32_PF, HEAL_STREAM32_LW,
+                                         HEAL_STREAM32_R>(a, stream);
+                if (a.M > 32 && a.M <= 64 && vec_path_applies<OP, 64, 16, HEAL_STREAM64_BK>(a))
+                    return launch_stream<OP, 64, HEAL_STREAM64_BK, HEAL_STREAM64_PF, HEAL_STREAM64_LW,
+                                         HEAL_STREAM64_R>(a, stream);
+            }
+        }
         if (a.M <= 16)
             return wide ? launch_cfg<OP, HEAL_OP_SKINNY16_CFG>(a, stream)
                         : launch_cfg<OP, HEAL_OP_NARROW16_CFG>(a, stream);

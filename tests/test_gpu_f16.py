@@ -586,3 +586,38 @@ def test_f16w_full_wide_weight_range(orc):
     C, e = run_f16w(A, W, 2)
     _, S = orc.gemm_f16w(A, W, e, 2)
     check_tolerance(C, S, f16w_absprod(orc, A, W, e), "wide weight range")
+
+
+@pytest.mark.parametrize("N,K", [(1040, 1028), (300, 40), (272, 4096)],
+                         ids=["ragged-n-ktail", "one-stage", "long-k"])
+def test_stream_tiles_every_m_bitwise(orc, N, K):
+    """Every row count 1..64 through the skinny instance of the packed-weight
+    products (the streamed narrow tiles of 16, 32 and 64 rows: a loader /
+    compute hand-over through a ring of LDS stages), with a ragged last
+    column block, a K tail, a single stage and a K that wraps the ring many
+    times: each row bitwise equal to the medium instance's row of the full
+    64-row product, and the 64-row results within the oracle's bars."""
+    A = wl.random_matrix((64, K), seed=N + K, sigma=2.0)
+    W = wl.random_matrix((N, K), seed=N + 3 * K, sigma=0.02)
+    e = heal.heal_f16_weight_exponent(float(np.abs(W).max()))
+    Ad, Wd = to_dev(A), to_dev(W)
+    W16 = heal.heal_pack_f16_weight(Wd, e)
+    Bp = heal.heal_presplit_b(Wd, trans_b=True)
+    for products in (1, 2):
+        announce("stream tiles every M, f16w p%d N=%d K=%d" % (products, N, K))
+        ref = heal.heal_gemm_f16w(Ad, W16, N, e, products, instance=heal.INSTANCE_MEDIUM)
+        torch.cuda.synchronize()
+        _, S = orc.gemm_f16w(A, W, e, products)
+        check_tolerance(ref.cpu().numpy(), S, f16w_absprod(orc, A, W, e), "p%d" % products)
+        for m in range(1, 65):
+            C = heal.heal_gemm_f16w(Ad[:m], W16, N, e, products, instance=heal.INSTANCE_SKINNY)
+            torch.cuda.synchronize()
+            assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), \
+                "p%d M=%d differs" % (products, m)
+    announce("stream tiles every M, pre-split N=%d K=%d" % (N, K))
+    ref = heal.heal_gemm_f32_presplit(Ad, Bp, N, instance=heal.INSTANCE_MEDIUM)
+    torch.cuda.synchronize()
+    for m in range(1, 65):
+        C = heal.heal_gemm_f32_presplit(Ad[:m], Bp, N, instance=heal.INSTANCE_SKINNY)
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "pre-split M=%d" % m
