@@ -13,11 +13,10 @@
 // columns for 4096-wide outputs) so that every CU streams its own share of
 // B: HBM bandwidth needs all CUs with loads in flight.
 //
-// Pipeline.  B is staged in a ring of R register sets: while stage s is
-// multiplied out of LDS, stage s+1 is split into the other LDS buffer and
-// its register set is reloaded with stage s+1+R, so each HBM load has R
-// stages to arrive.
-// A (L2 hits) is staged one stage ahead.  Split, LDS layout and fragment
+// Pipeline.  A and B are staged in a ring of R register sets: while stage s
+// is multiplied out of LDS, stage s+1 is split into the other LDS buffer and
+// its register set is reloaded with stage s+1+R, so each load (HBM for B,
+// mostly L2 for A) has R stages to arrive.  Split, LDS layout and fragment
 // reads follow the large kernel: 16-byte buffer loads, 4x4 register
 // transposes of B stored K x N, hi and lo planes with k-contiguous rows,
 // 16x16x32 bf16 MFMA fragments.  Lanes outside the matrix read zeros through
@@ -103,8 +102,8 @@ constexpr int skinny_occupancy(int MB, int CB, int BK)
 }
 
 // MB: 16-row blocks of the tile (M <= 16*MB); CB: 16-column blocks per
-// workgroup; BK: stage depth; R: depth of the B register ring (stages in
-// flight from HBM), even; NT: threads (all load and split; the first
+// workgroup; BK: stage depth; R: depth of the A and B register ring (stages in
+// flight), even; NT: threads (all load and split; the first
 // min(CB, 4) waves also multiply).
 template <int MB, int CB, int BK, int R, int NT, bool TRANS_B, bool ALPHA, bool TAIL>
 __global__ void __launch_bounds__(NT, skinny_occupancy(MB, CB, BK))
@@ -235,15 +234,15 @@ gemm_skinny_kernel(GemmArgs p)
         }
         const int ldb4 = (int)(p.ldb * 4);
 
-        f32x4 xa[NA];        // staged A (one stage)
-        f32x4 xb[R][NB];     // staged B (R stages, set = stage % R)
+        f32x4 xa[R][NA];     // staged A and B: R stages, set = stage % R
+        f32x4 xb[R][NB];
 
-        auto load_a = [&](int s) {
+        auto load_a = [&](int set, int s) {
 #pragma unroll
             for (int u = 0; u < NA; ++u) {
                 uint32_t v = va[u];
                 if (TAIL && s * BK + 4 * a_kq[u] >= k_end) v = kOOB;
-                xa[u] = bload(ra_src, v, s * BK * 4);
+                xa[set][u] = bload(ra_src, v, s * BK * 4);
             }
         };
         auto load_b = [&](int set, int s) {
@@ -261,12 +260,12 @@ gemm_skinny_kernel(GemmArgs p)
                 }
             }
         };
-        auto split_a = [&](char *st) {
+        auto split_a = [&](char *st, int set) {
 #pragma unroll
             for (int u = 0; u < NA; ++u) {
                 uint32_t h0, l0, h1, l1;
-                split2(xa[u].x, xa[u].y, h0, l0);
-                split2(xa[u].z, xa[u].w, h1, l1);
+                split2(xa[set][u].x, xa[set][u].y, h0, l0);
+                split2(xa[set][u].z, xa[set][u].w, h1, l1);
                 lds_store2(st, st_a[u], h0, h1);
                 lds_store2(st + A_PLANE, st_a[u], l0, l1);
             }
@@ -349,38 +348,52 @@ gemm_skinny_kernel(GemmArgs p)
             }
         };
 
+        // Stage t lives in register set t % R.  At step s stage s is
+        // multiplied out of LDS buffer s & 1 while the set of stage s+1 is
+        // split into the other buffer and then reloaded with stage s+1+R, so
+        // each HBM load has R steps to arrive.  Reloads past the last stage
+        // are clamped to it (redundant loads whose data is never used).  The
+        // loop is unrolled by R (R even), so that register sets and LDS
+        // buffers are compile-time choices, and every group of R steps runs
+        // whole: only the multiply of a step past the last stage is skipped.
+        // With a step under a branch the compiler has to assume a path
+        // around it and waits for every outstanding load before the split
+        // (vmcnt(0)), which halves the depth of the ring.
+        static_assert(R % 2 == 0, "register sets come in pairs");
         const int last = ns - 1;
+        auto clamp = [&](int t) { return t < last ? t : last; };
+        auto load_set = [&](int set, int s) {
+            load_a(set, s);
+            load_b(set, s);
+        };
         if (ns > 0) {
-            // prologue: stage 0 into buffer 0; A stage 1 and B stages 1..R staged
-            load_a(0);
-            load_b(0, 0);
-            split_a(smem);
+            load_set(0, 0);
+            split_a(smem, 0);
             split_b(smem, 0);
-            load_a(1 < last ? 1 : last);
+            // the sets are issued in ring order (scheduling barriers keep the
+            // compiler from interleaving them), the order the loop keeps, so
+            // that every wait before a split is exact
 #pragma unroll
-            for (int t = 1; t <= R; ++t) load_b(t % R, t < last ? t : last);
+            for (int t = 1; t < R; ++t) {
+                __builtin_amdgcn_sched_barrier(0);
+                load_set(t, clamp(t));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            load_set(0, clamp(R));
+            __builtin_amdgcn_sched_barrier(0);
             __syncthreads();
         }
-        // main loop, R stages per trip so that LDS buffers and register sets
-        // are compile-time choices.  Stage s is multiplied out of buffer s&1
-        // while stage s+1 (register set (s+1)%R) is split into the other
-        // buffer; that set is then reloaded with stage s+1+R, so each HBM
-        // load has R stages to arrive.  Reload stages are clamped to the last
-        // stage (redundant loads, never used).
         for (int s0 = 0; s0 < ns; s0 += R) {
 #pragma unroll
             for (int t = 0; t < R; ++t) {
                 const int s = s0 + t;
-                if (t == 0 || s < ns) {
-                    char *cur = smem + (t & 1) * STAGE;
-                    char *nxt = smem + ((t + 1) & 1) * STAGE;
-                    compute(cur);
-                    split_a(nxt);
-                    split_b(nxt, (t + 1) % R);
-                    load_a(s + 2 < last ? s + 2 : last);
-                    load_b((t + 1) % R, s + 1 + R < last ? s + 1 + R : last);
-                    __syncthreads();
-                }
+                char *cur = smem + (t & 1) * STAGE;
+                char *nxt = smem + ((t + 1) & 1) * STAGE;
+                if (s < ns) compute(cur);
+                split_a(nxt, (t + 1) % R);
+                split_b(nxt, (t + 1) % R);
+                load_set((t + 1) % R, clamp(s + 1 + R));
+                __syncthreads();
             }
         }
 
@@ -435,9 +448,11 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 // still beats 128 wider ones at every row count (32 rows: 27 vs 29 us; 64
 // rows: 38 vs 41 us); wide outputs (lm_head) use 256-column strips.  The
 // stage depth is the smallest that gives every thread whole 16-byte units
-// of A and B at the tile's row count.  Narrow strips run 512 threads (half
-// blocks of B): 64 rows 33.6 vs 37.6 us with 256, 1 to 32 rows the same or
-// slightly faster.  Wide strips (lm_head, 64 x 128256 x 4096, with 16, 32
+// of A and B at the tile's row count.  Narrow strips of 64 rows run 512
+// threads (half blocks of B; 33.6 vs 37.6 us with 256), of 17 to 32 rows
+// 256 threads (25.7 vs 26.5 us with 512), of 16 rows either (22.6 us; a
+// read-only kernel of the same B pattern takes 17.5 us, 20.5 us when it
+// also reads A from L2 as every workgroup here does).  Wide strips (lm_head, 64 x 128256 x 4096, with 16, 32
 // or 64 rows): 256 columns everywhere, 512 threads where every thread still
 // gets whole A quads: 0.43 / 0.40 / 0.37 ms against 0.55 / 0.45 / 0.39 ms
 // for the earlier 128-column strips at 16 and 32 rows and 256 threads.
@@ -445,7 +460,7 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 #define HEAL_SKINNY_N1 1, 256, 2, 512      // M <= 16, narrow: CB, BK, R, NT
 #endif
 #ifndef HEAL_SKINNY_N2
-#define HEAL_SKINNY_N2 1, 256, 2, 512
+#define HEAL_SKINNY_N2 1, 128, 2, 256
 #endif
 #ifndef HEAL_SKINNY_N4
 #define HEAL_SKINNY_N4 1, 256, 2, 512      // 160 KB of LDS: one workgroup per CU
