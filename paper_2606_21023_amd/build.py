@@ -18,7 +18,7 @@ LIBRARY = os.path.join(PKG, "libheal.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["heal_api.cpp", "heal_split.hip", "heal_gemm.hip", "heal_gemm_large.hip",
-           "heal_gemm_skinny.hip", "heal_ops.hip", "heal_gemm_op.hip"]
+           "heal_gemm_skinny.hip", "heal_gemm_panel.hip", "heal_ops.hip", "heal_gemm_op.hip"]
 
 # Packed FP32 instructions are disabled: only plain FP32 VALU code is emitted.
 # The host pass of hipcc does not know this feature and says so; harmless.

@@ -525,9 +525,11 @@ hipError_t launch_gemm(int instance, const GemmArgs &a, bool trans_b, bool use_a
 {
     switch (instance) {
     case HEAL_INSTANCE_LARGE:
+        if (HEAL_PANEL && panel_kernel_applies(a, trans_b)) return launch_gemm_panel(a, use_alpha, stream);
         if (large_kernel_applies(a, trans_b)) return launch_gemm_large(a, trans_b, use_alpha, stream);
         return launch_tile<HEAL_LARGE_CFG>(a, trans_b, use_alpha, stream);
     case HEAL_INSTANCE_MEDIUM:
+        if (HEAL_PANEL && panel_kernel_applies(a, trans_b)) return launch_gemm_panel(a, use_alpha, stream);
         return launch_tile<HEAL_MEDIUM_CFG>(a, trans_b, use_alpha, stream);
     case HEAL_INSTANCE_SKINNY:
         if (skinny_kernel_applies(a, trans_b)) return launch_gemm_skinny(a, trans_b, use_alpha, stream);

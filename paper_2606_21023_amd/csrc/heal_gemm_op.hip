@@ -1350,6 +1350,10 @@ hipError_t launch_large(const OpArgs &a, hipStream_t stream)
 template <int OP>
 hipError_t launch_op(int instance, const OpArgs &a, hipStream_t stream)
 {
+    if constexpr (OP == OP_SCORES) {
+        if (HEAL_PANEL && instance != HEAL_INSTANCE_SKINNY && scores_panel_applies(a))
+            return launch_scores_panel(a, stream);
+    }
     switch (instance) {
     case HEAL_INSTANCE_LARGE: return launch_large<OP>(a, stream);
     case HEAL_INSTANCE_MEDIUM: return launch_cfg<OP, HEAL_OP_MEDIUM_CFG>(a, stream);

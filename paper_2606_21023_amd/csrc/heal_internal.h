@@ -38,6 +38,17 @@ bool skinny_kernel_applies(const GemmArgs &args, bool trans_b);
 hipError_t launch_gemm_skinny(const GemmArgs &args, bool trans_b, bool use_alpha,
                               hipStream_t stream);
 
+// The short-K panel kernel (heal_gemm_panel.hip): B stored N x K, K <= 128,
+// 16-byte rows, at least one panel of rows (256 for bf16x3, 128 for the
+// scores); a panel of A stays in LDS while the workgroup walks the columns
+// of C (attention scores).  HEAL_PANEL 0
+// keeps those products on the tiled kernels.
+#ifndef HEAL_PANEL
+#define HEAL_PANEL 1
+#endif
+bool panel_kernel_applies(const GemmArgs &args, bool trans_b);
+hipError_t launch_gemm_panel(const GemmArgs &args, bool use_alpha, hipStream_t stream);
+
 hipError_t launch_split(const float *x, uint16_t *hi, uint16_t *lo, int64_t n, hipStream_t stream);
 
 // ---- FP16 / INT16 forms and the pre-split operand (heal_ops.hip, heal_gemm_op.hip) ----
@@ -65,6 +76,10 @@ struct OpArgs {
     float alpha;                // SCORES
     int vecA, vecB, vecC;       // 16-byte rows (pointer, leading dimension, batch stride)
 };
+
+// The INT16 scores on the short-K panel kernel (heal_gemm_panel.hip).
+bool scores_panel_applies(const OpArgs &args);
+hipError_t launch_scores_panel(const OpArgs &args, hipStream_t stream);
 
 // instance: HEAL_INSTANCE_* (AUTO chooses from M and N).
 hipError_t launch_gemm_op(int op, int instance, const OpArgs &args, hipStream_t stream);
