@@ -15,9 +15,12 @@ Prints ONE JSON line:
                  hbm:  FP32 A, B read once and C written once per launch over
                        the 8 TB/s HBM peak;
                the launches of the timed region run back to back on one
-               stream (pre-built C-ABI arguments, no per-call marshalling);
-               the launch duration is the HIP-event time of the region on
-               that stream divided by the number of launches.  traffic is
+               stream (pre-built C-ABI arguments, no per-call marshalling;
+               --graph captures them into one HIP graph and times one replay
+               of it, for microsecond kernels under a tracer, whose host
+               cost per launch would leave gaps); the launch duration is the
+               HIP-event time of the region on that stream divided by the
+               number of launches.  traffic is
                the HBM bytes per launch measured by FETCH_SIZE / WRITE_SIZE
                counters (scaled by a plain copy of known size), taken from
                profiles/traffic.json only while the kernel sources are the
@@ -28,8 +31,11 @@ Prints ONE JSON line:
                them); all are compared bitwise with the first timed output
   build_id     the source hash libheal.so was built from (checked at start)
   step_stats   median, minimum and standard error of the per-launch times
-               of a second pass of the same launches with an event between
-               each (the paper's timing convention), after the timed region
+               of a separate pass of the same launches with an event between
+               each (the paper's timing convention), run before the warm-up
+               launches; the FP32 comparison (below) runs before it.  Both
+               take the GPU out of its idle clocks, which would otherwise
+               slow the first tens of launches
 
 --method selects the product (default bf16x3, the line above):
   presplit    heal_gemm_f32_presplit: B split once into packed bf16 (hi, lo)
@@ -46,7 +52,7 @@ For every GEMM method a step is one launch of its GEMM kernel over the
 workload; value is FP32-equivalent TFLOP/s (2*M*N*K*batch per step); the
 roofline uses the method's own MFMA flops and operand bytes.
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--method NAME] [--no-cpu]
+                       [--method NAME] [--no-cpu] [--graph]
 """
 import argparse
 import hashlib
@@ -98,6 +104,11 @@ def parse():
     ap.add_argument("--workload", default="square8192")
     ap.add_argument("--method", default="bf16x3", choices=sorted(METHODS))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the K timed launches into one HIP graph and time one replay "
+                         "of it, instead of issuing them one by one from Python (for "
+                         "microsecond kernels under a tracer, whose per-launch host cost "
+                         "would otherwise leave gaps between them)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the CPU oracle sample")
     ap.add_argument("--profile-summary", metavar="DIR",
@@ -189,9 +200,9 @@ def cpu_baseline(w, A, B, target_s, method="bf16x3", extra=None):
 
 def step_stats(run, steps, stream):
     """Per-launch durations from one HIP event before and after every launch,
-    in a pass of its own after the timed region (so that the timed region
-    holds nothing but the launches): median, minimum and standard error of
-    the mean, in ms."""
+    in a pass of its own before the warm-up launches (so that the timed
+    region holds nothing but the launches): median, minimum and standard
+    error of the mean, in ms."""
     import torch
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     ev[0].record(stream)
@@ -203,6 +214,20 @@ def step_stats(run, steps, stream):
     sem = float(d.std(ddof=1) / math.sqrt(len(d))) if len(d) > 1 else 0.0
     return {"launches": steps, "median_ms": round(float(np.median(d)), 5),
             "min_ms": round(float(d.min()), 5), "sem_ms": round(sem, 6)}
+
+
+def graph_of(steps, launch):
+    """A HIP graph holding `steps` launches: launch(i, stream) issues launch
+    i on the given stream (the capture stream while capturing)."""
+    import ctypes
+    import torch
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        cs = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        for i in range(steps):
+            launch(i, cs)
+    torch.cuda.synchronize()
+    return g
 
 
 def bench_split(args, w):
@@ -231,24 +256,30 @@ def bench_split(args, w):
     stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
     calls = [(xs[i % n_rot].data_ptr(), outs[i % n_out][0].data_ptr(),
-              outs[i % n_out][1].data_ptr(), n, sp)
+              outs[i % n_out][1].data_ptr(), n)
              for i in range(max(args.steps, args.warmup, 1))]
 
-    def run(i):
-        st = L.heal_split_f32(*calls[i % len(calls)])
+    def run(i, s=sp):
+        st = L.heal_split_f32(*calls[i % len(calls)], s)
         if st != 0:
             raise heal.HealError("launch failed with status %d" % st)
 
-    # dispatch order: warmup launches, timed launches, statistics pass
+    # dispatch order: statistics pass, warmup launches, timed launches (the
+    # statistics pass first also takes the GPU out of its idle clocks)
+    stats = step_stats(run, args.steps, stream)
     for i in range(args.warmup):
         run(i)
     torch.cuda.synchronize()
+    g = graph_of(args.steps, run) if args.graph else None
     e_start = torch.cuda.Event(enable_timing=True)
     e_end = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e_start.record(stream)
-    for i in range(args.steps):
-        run(i)
+    if g is not None:
+        g.replay()
+    else:
+        for i in range(args.steps):
+            run(i)
     e_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -256,7 +287,6 @@ def bench_split(args, w):
     identical = all(torch.equal(outs[j][0], outs[0][0]) and torch.equal(outs[j][1], outs[0][1])
                     for j in range(1, n_cmp))
     ms = e_start.elapsed_time(e_end) / args.steps
-    stats = step_stats(run, args.steps, stream)
     gbs = alg_bytes / (ms * 1e-3) / 1e9
     traffic = measured_traffic("split:%s" % w.name, "split")
     roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -296,6 +326,8 @@ def bench_split(args, w):
         "data": "synthetic",
         "config": {"workload": w.name, "method": "split", "elements": n,
                    "inputs": "the B operand of: " + w.note, "operand_copies_rotated": n_rot},
+        "timing": ("one replay of a HIP graph holding the K launches" if args.graph
+                   else "K launches issued one by one"),
         "bit_repro": {"runs": n_cmp, "identical": identical,
                       "compared": ("both planes of every timed launch" if n_cmp == args.steps
                                    else "both planes of the last %d timed launches" % n_cmp)
@@ -319,10 +351,10 @@ def bench_split(args, w):
 def _kernel_base_name(full):
     """`void heal::(anonymous namespace)::gemm_large8_kernel<...>(...)` ->
     `gemm_large8_kernel`."""
-    n = full.split("(anonymous namespace)::")[-1]
+    n = full.replace("(anonymous namespace)::", "").replace("void ", "", 1)
     for stop in ("<", "("):
         n = n.split(stop)[0]
-    return n.replace("void ", "").strip()
+    return n.split("::")[-1].strip()
 
 
 def profile_summary(d, out=None):
@@ -336,7 +368,7 @@ def profile_summary(d, out=None):
                         run with --copy-calibration (optional);
       DIR/p3/           --pmc of SQ and GRBM counters (optional).
     The measured kernel is the one the JSON line names; its dispatches come
-    in the order of this script (warm-up, timed, statistics pass), so the
+    in the order of this script (statistics pass, warm-up, timed), so the
     average over the timed dispatches alone is reported next to the HIP-event
     time of the same launches.  With `out` (a path under profiles/) the
     summary is written there and the HBM bytes per launch go into
@@ -366,7 +398,7 @@ def profile_summary(d, out=None):
                                                                          W + 2 * K)
     dur = np.array([int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in disp],
                    np.float64)
-    timed, second = dur[W:W + K], dur[W + K:]
+    second, timed = dur[:K], dur[K + W:]
     stats = rows("trace/*kernel_stats.csv")
     full = disp[0]["Kernel_Name"]
     L = ["# %s, %s, workload %s\n" % (kname, cfg["method"], cfg["workload"])]
@@ -385,8 +417,9 @@ def profile_summary(d, out=None):
                                                         float(r["Percentage"])))
     L.append("\nFull name of the measured kernel: `%s`\n" % full)
     L.append("## The timed launches\n")
-    L.append("Dispatches of the measured kernel in the traced process: %d warm-up, %d timed, "
-             "%d of the per-launch statistics pass (%d in all).\n" % (W, K, K, len(disp)))
+    L.append("Dispatches of the measured kernel in the traced process, in order: %d of the "
+             "per-launch statistics pass, %d warm-up, %d timed (%d in all).\n"
+             % (K, W, K, len(disp)))
     L.append("| source | launches | mean us | min us | max us |")
     L.append("|---|---|---|---|---|")
     L.append("| bench.py HIP events, timed region / launches | %d | %.2f | | |"
@@ -396,7 +429,7 @@ def profile_summary(d, out=None):
     L.append("| rocprofv3, the statistics pass | %d | %.2f | %.2f | %.2f |"
              % (K, second.mean() / 1e3, second.min() / 1e3, second.max() / 1e3))
     L.append("| rocprofv3, warm-up dispatches | %d | %s | | |"
-             % (W, "%.2f" % (dur[:W].mean() / 1e3) if W else "-"))
+             % (W, "%.2f" % (dur[K:K + W].mean() / 1e3) if W else "-"))
     rl = line["roofline"]
     per = rl["achieved"] * rl["avg_launch_us"]            # algorithmic units per launch x us
     frac_trace = per / (timed.mean() / 1e3) / rl["peak"]
@@ -450,6 +483,33 @@ def profile_summary(d, out=None):
             L.append("\nMFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 "
                      "SIMDs) = %.3f; clock = GRBM_GUI_ACTIVE / 8 / trace mean = %.2f GHz.\n"
                      % (busy / (act / 8 * 1024), act / 8 / timed.mean()))
+    # further counter passes (DIR/p4, DIR/p5, ...): cache, request-size and
+    # latency counters of the measured kernel
+    extra = {}
+    for sub in sorted(glob.glob(os.path.join(d, "p[4-9]"))):
+        for r in rows(os.path.join(os.path.basename(sub), "*counter_collection.csv")):
+            if _kernel_base_name(r["Kernel_Name"]) == kname:
+                extra.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    if extra:
+        L.append("## Cache, request-size and latency counters, mean per dispatch\n")
+        L.append("| counter | mean | dispatches |")
+        L.append("|---|---|---|")
+        for c in sorted(extra):
+            L.append("| %s | %.6g | %d |" % (c, np.mean(extra[c]), len(extra[c])))
+        m = {c: np.mean(v) for c, v in extra.items()}
+        notes = []
+        if "TCC_HIT_sum" in m and "TCC_MISS_sum" in m:
+            notes.append("L2 hit rate TCC_HIT / (TCC_HIT + TCC_MISS) = %.3f"
+                         % (m["TCC_HIT_sum"] / max(1.0, m["TCC_HIT_sum"] + m["TCC_MISS_sum"])))
+        if "TCC_EA0_RDREQ_sum" in m and "TCC_EA0_RDREQ_128B_sum" in m:
+            notes.append("share of L2-to-memory read requests that are 128-byte: %.3f"
+                         % (m["TCC_EA0_RDREQ_128B_sum"] / max(1.0, m["TCC_EA0_RDREQ_sum"])))
+        if "TCP_TCC_READ_REQ_LATENCY_sum" in m and "TCP_TCC_READ_REQ_sum" in m:
+            notes.append("mean L1-to-L2 read latency TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ "
+                         "= %.0f cycles" % (m["TCP_TCC_READ_REQ_LATENCY_sum"]
+                                            / max(1.0, m["TCP_TCC_READ_REQ_sum"])))
+        if notes:
+            L.append("\n" + "; ".join(notes) + ".\n")
     L.append("## bench.py line of the traced run\n")
     L.append("```\n%s\n```" % line_text)
     text = "\n".join(L) + "\n"
@@ -460,7 +520,8 @@ def profile_summary(d, out=None):
         f.write(text)
     if traffic is not None:
         inst = {"bf16x3": None, "split": "split"}.get(cfg["method"], "op")
-        if panel_applies(cfg["method"], cfg["M"], cfg["N"], cfg["K"], cfg.get("trans_b", False)):
+        if cfg["method"] != "split" and panel_applies(cfg["method"], cfg["M"], cfg["N"], cfg["K"],
+                                                      cfg.get("trans_b", False)):
             inst = "panel"
         elif inst is None:
             import paper_2606_21023_amd as heal
@@ -562,6 +623,29 @@ def main():
     outs = [torch.zeros(c_shape, dtype=torch.float32, device=dev) for _ in range(n_out)]
     torch.cuda.synchronize()
 
+    # MI355X native FP32 GEMM on the same (FP32) inputs, TF32 off; it runs
+    # first, so that the GPU has left its idle clocks before the warm-up
+    # launches of the product (a few warm-up launches of a 2 ms kernel are
+    # otherwise still on the clock ramp)
+    torch.backends.cuda.matmul.allow_tf32 = False
+    torch.set_float32_matmul_precision("highest")
+    Af, Bf = torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
+    mm = (lambda: torch.matmul(Af, Bf.transpose(-1, -2))) if w.trans_b else (lambda: Af @ Bf)
+    for _ in range(3):
+        mm()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = max(3, min(20, args.steps))
+    e0.record(torch.cuda.current_stream())
+    for _ in range(reps):
+        mm()
+    e1.record(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    native_ms = e0.elapsed_time(e1) / reps
+    comparison = {"torch_fp32_matmul_tflops": round(w.flops / (native_ms * 1e-3) / 1e12, 2),
+                  "torch_fp32_matmul_ms": round(native_ms, 4)}
+    del Af, Bf
+
     # Launch through the C ABI with pre-built arguments, so that the timed
     # loop measures the kernels rather than argument marshalling: every step
     # is one library call on the current stream.
@@ -576,44 +660,56 @@ def main():
         if method == "i16_scores":
             cargs = (w.M, w.N, w.K, Ad.data_ptr(), w.K, w.M * w.K, st[2].data_ptr(), Bd.data_ptr(),
                      w.K, w.N * w.K, st[3].data_ptr(), ctypes.c_float(w.alpha), Cd.data_ptr(),
-                     w.N, w.M * w.N, w.batch, sp)
+                     w.N, w.M * w.N, w.batch)
             return L.heal_scores_i16, cargs
         if method in ("f16_full", "f16_base"):
             cargs = (meta["products"], w.M, w.N, w.K, Ad.data_ptr(), w.K, Bd.data_ptr(),
-                     extra["e"], Cd.data_ptr(), w.N, sp)
+                     extra["e"], Cd.data_ptr(), w.N)
             return L.heal_gemm_f16w, cargs
         if method == "presplit":
-            cargs = (w.M, w.N, w.K, Ad.data_ptr(), w.K, Bd.data_ptr(), Cd.data_ptr(), w.N, sp)
+            cargs = (w.M, w.N, w.K, Ad.data_ptr(), w.K, Bd.data_ptr(), Cd.data_ptr(), w.N)
             return L.heal_gemm_f32_presplit, cargs
         if batched:
             lda, ldb, ldc = w.K, (w.K if w.trans_b else w.N), w.N
             cargs = (w.M, w.N, w.K, ctypes.c_float(w.alpha), Ad.data_ptr(), lda, w.M * w.K,
                      Bd.data_ptr(), ldb, w.N * w.K, 1 if w.trans_b else 0, Cd.data_ptr(), ldc,
-                     w.M * w.N, w.batch, sp)
+                     w.M * w.N, w.batch)
             return L.heal_gemm_f32_strided_batched, cargs
-        cargs = (w.M, w.N, w.K, Ad.data_ptr(), Bd.data_ptr(), Cd.data_ptr(), w.K, w.N, w.N, sp)
+        cargs = (w.M, w.N, w.K, Ad.data_ptr(), Bd.data_ptr(), Cd.data_ptr(), w.K, w.N, w.N)
         return L.heal_gemm_f32, cargs
 
     calls = [make_call(i) for i in range(max(args.steps, args.warmup, 1))]
 
-    def run(i):
+    def run(i, s=sp):
         fn, cargs = calls[i % len(calls)]
-        st = fn(*cargs)
+        st = fn(*cargs, s)
         if st != 0:
             raise heal.HealError("launch failed with status %d" % st)
 
-    # dispatch order of the kernel: warmup launches, the timed launches, then
-    # the launches of the per-launch statistics pass
+    # dispatch order of the kernel: the launches of the per-launch statistics
+    # pass, the warm-up launches, the timed launches.  The FP32 comparison
+    # and the statistics pass before the warm-up take the GPU out of its
+    # idle clocks: after ~40 ms idle an 8192^3 launch takes 2.5-3.2 ms and
+    # settles near 2.2 ms only after some 50-100 ms of back-to-back work.
+    stats = step_stats(run, args.steps, stream)
     for i in range(args.warmup):
         run(i)
     torch.cuda.synchronize()
+    # --graph: the timed launches captured once into a HIP graph (not timed),
+    # so that the timed region is the kernels back to back rather than the
+    # rate at which Python issues them (graph replays measured 1-3% slower
+    # than eager launches for the millisecond kernels)
+    g = graph_of(args.steps, run) if args.graph else None
 
     e_start = torch.cuda.Event(enable_timing=True)
     e_end = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e_start.record(stream)
-    for i in range(args.steps):
-        run(i)
+    if g is not None:
+        g.replay()
+    else:
+        for i in range(args.steps):
+            run(i)
     e_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -622,7 +718,6 @@ def main():
     ref = outs[0].view(torch.int32)
     identical = all(bool(torch.equal(outs[j].view(torch.int32), ref)) for j in range(1, n_cmp))
     total_ms = e_start.elapsed_time(e_end)
-    stats = step_stats(run, args.steps, stream)
     ms_per_step = total_ms / args.steps
     # launches run back to back on one stream: the mean launch duration is
     # the timed region over the number of launches
@@ -646,7 +741,12 @@ def main():
         traffic = measured_traffic("%s:%s" % (method, w.name), "op")
         label = OP_INSTANCE_NAMES.get(instance, "?")
         kname = "gemm_op_kernel"
-        if instance == 1 and method != "i16_scores":
+        if instance == 3 and method != "i16_scores" and -(-w.N // 256) < 384:
+            # M <= 64 with fewer than 384 256-column tiles: the streamed
+            # narrow tiles (loader waves and one computing wave, 16 columns)
+            kname = "gemm_op_stream_kernel"
+            label = "narrow 16-column tiles, loader waves + one MFMA wave, LDS ring"
+        elif instance == 1 and method != "i16_scores":
             # 16-byte aligned rows: the hand-scheduled kernel, 224 columns
             # where that takes fewer rounds of one workgroup per CU
             cus = torch.cuda.get_device_properties(0).multi_processor_count
@@ -674,26 +774,6 @@ def main():
     roofline.update({"traffic": None if traffic is None else round(traffic),
                      "kernel": kernel, "per_launch": per_launch,
                      "avg_launch_us": round(avg_launch_ms * 1e3, 2)})
-
-    # MI355X native FP32 GEMM on the same (FP32) inputs, TF32 off
-    torch.backends.cuda.matmul.allow_tf32 = False
-    torch.set_float32_matmul_precision("highest")
-    Af, Bf = torch.from_numpy(A).to(dev), torch.from_numpy(B).to(dev)
-    mm = (lambda: torch.matmul(Af, Bf.transpose(-1, -2))) if w.trans_b else (lambda: Af @ Bf)
-    for _ in range(3):
-        mm()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = max(3, min(20, args.steps))
-    e0.record(stream)
-    for _ in range(reps):
-        mm()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    native_ms = e0.elapsed_time(e1) / reps
-    comparison = {"torch_fp32_matmul_tflops": round(flops / (native_ms * 1e-3) / 1e12, 2),
-                  "torch_fp32_matmul_ms": round(native_ms, 4)}
-    del Af, Bf
 
     cpu = None
     if not args.no_cpu:
@@ -727,6 +807,8 @@ def main():
                    "inputs": w.note, "operand_copies_rotated": n_rot},
         "pct_of_bf16_peak_div3": round(100.0 * value / (BF16_DENSE_PEAK_TFLOPS / 3), 2),
         "hbm_gbs": round(alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "timing": ("one replay of a HIP graph holding the K launches" if args.graph
+                   else "K launches issued one by one"),
         "bit_repro": {"runs": n_cmp, "identical": identical,
                       "compared": ("whole output of every timed launch" if n_cmp == args.steps
                                    else "whole output of the last %d timed launches" % n_cmp)

@@ -61,12 +61,12 @@ def _write_csv(path, header, rows):
 
 def test_profile_summary_averages_the_timed_dispatches(tmp_path):
     """--profile-summary on a synthetic rocprofv3 directory: the measured
-    kernel's dispatches are split into warm-up, timed and statistics-pass
+    kernel's dispatches are split into statistics-pass, warm-up and timed
     launches by order, and the timed average and traffic come out right."""
     W, K = 2, 3
     name = "void heal::(anonymous namespace)::gemm_large8_kernel<false, false, false>(heal::GemmArgs)"
-    # warm-up launches 5 us, timed 2 us, statistics pass 3 us; another kernel in between
-    durs = [5000] * W + [2000] * K + [3000] * K
+    # statistics pass 3 us, warm-up launches 5 us, timed 2 us; another kernel in between
+    durs = [3000] * K + [5000] * W + [2000] * K
     trace, t = [], 1000
     for i, d in enumerate(durs):
         trace.append(["KERNEL_DISPATCH", "Agent 1", 1, 0, 1, 2 * i + 1, 7, name, 1, t, t + d])

@@ -198,7 +198,10 @@ def test_config_attention_sampled(orc):
         Cr = C[h][torch.from_numpy(rows).cuda()].cpu().numpy()
         B = np.ascontiguousarray(Kh[h].T)
         _, S = orc.gemm3(Q[h], B, alpha=w.alpha, rows=rows)
-        check_tolerance(Cr, alpha * S, alpha * abs_product(Q[h][rows], B), "attn head %d" % h)
+        nw, ew = check_tolerance(Cr, alpha * S, alpha * abs_product(Q[h][rows], B),
+                                 "attn head %d" % h)
+        print("attn_scores head %d rows %s normwise %.3g elementwise %.3g" % (h, rows.tolist(), nw,
+                                                                            ew))
 
 
 # ---------------------------------------------------------------------------
