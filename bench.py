@@ -329,9 +329,10 @@ def bench_split(args, w):
         "timing": ("one replay of a HIP graph holding the K launches" if args.graph
                    else "K launches issued one by one"),
         "bit_repro": {"runs": n_cmp, "identical": identical,
-                      "compared": ("both planes of every timed launch" if n_cmp == args.steps
-                                   else "both planes of the last %d timed launches" % n_cmp)
-                      + " (one buffer pair each) against the first"},
+                      "compared": ("both planes of every timed launch (one buffer pair each) "
+                                   "against the first" if n_cmp == args.steps
+                                   else "both planes of the last %d timed launches (one buffer "
+                                   "pair each, reused in turn) against each other" % n_cmp)},
         "step_stats": stats,
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -810,9 +811,10 @@ def main():
         "timing": ("one replay of a HIP graph holding the K launches" if args.graph
                    else "K launches issued one by one"),
         "bit_repro": {"runs": n_cmp, "identical": identical,
-                      "compared": ("whole output of every timed launch" if n_cmp == args.steps
-                                   else "whole output of the last %d timed launches" % n_cmp)
-                      + " (one buffer each) against the first"},
+                      "compared": ("whole output of every timed launch (one buffer each) "
+                                   "against the first" if n_cmp == args.steps
+                                   else "whole output of the last %d timed launches (one buffer "
+                                   "each, reused in turn) against each other" % n_cmp)},
         "step_stats": stats,
         "roofline": roofline,
         "cpu_baseline": cpu,
