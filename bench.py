@@ -201,19 +201,24 @@ def cpu_baseline(w, A, B, target_s, method="bf16x3", extra=None):
 def step_stats(run, steps, stream):
     """Per-launch durations from one HIP event before and after every launch,
     in a pass of its own before the warm-up launches (so that the timed
-    region holds nothing but the launches): median, minimum and standard
-    error of the mean, in ms."""
+    region holds nothing but the launches).  Returns a function that, once
+    the stream has drained, gives the median, minimum and standard error of
+    the mean in ms: the pass does not wait for the GPU, so the warm-up
+    launches follow it without an idle gap (a few ms idle put the clock
+    back on its ramp)."""
     import torch
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     ev[0].record(stream)
     for i in range(steps):
         run(i)
         ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    d = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)], dtype=np.float64)
-    sem = float(d.std(ddof=1) / math.sqrt(len(d))) if len(d) > 1 else 0.0
-    return {"launches": steps, "median_ms": round(float(np.median(d)), 5),
-            "min_ms": round(float(d.min()), 5), "sem_ms": round(sem, 6)}
+
+    def result():
+        d = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)], dtype=np.float64)
+        sem = float(d.std(ddof=1) / math.sqrt(len(d))) if len(d) > 1 else 0.0
+        return {"launches": steps, "median_ms": round(float(np.median(d)), 5),
+                "min_ms": round(float(d.min()), 5), "sem_ms": round(sem, 6)}
+    return result
 
 
 def graph_of(steps, launch):
@@ -333,7 +338,7 @@ def bench_split(args, w):
                                    "against the first" if n_cmp == args.steps
                                    else "both planes of the last %d timed launches (one buffer "
                                    "pair each, reused in turn) against each other" % n_cmp)},
-        "step_stats": stats,
+        "step_stats": stats(),
         "roofline": roofline,
         "cpu_baseline": cpu,
         "build_id": heal.build_id(),
@@ -641,10 +646,12 @@ def main():
     for _ in range(reps):
         mm()
     e1.record(torch.cuda.current_stream())
-    torch.cuda.synchronize()
-    native_ms = e0.elapsed_time(e1) / reps
-    comparison = {"torch_fp32_matmul_tflops": round(w.flops / (native_ms * 1e-3) / 1e12, 2),
-                  "torch_fp32_matmul_ms": round(native_ms, 4)}
+    # no wait here: the product's launches queue behind these, so the GPU
+    # does not idle in between; the time is read after the timed region
+    def native():
+        ms = e0.elapsed_time(e1) / reps
+        return {"torch_fp32_matmul_tflops": round(w.flops / (ms * 1e-3) / 1e12, 2),
+                "torch_fp32_matmul_ms": round(ms, 4)}
     del Af, Bf
 
     # Launch through the C ABI with pre-built arguments, so that the timed
@@ -690,8 +697,10 @@ def main():
     # dispatch order of the kernel: the launches of the per-launch statistics
     # pass, the warm-up launches, the timed launches.  The FP32 comparison
     # and the statistics pass before the warm-up take the GPU out of its
-    # idle clocks: after ~40 ms idle an 8192^3 launch takes 2.5-3.2 ms and
-    # settles near 2.2 ms only after some 50-100 ms of back-to-back work.
+    # idle clocks, and nothing waits for the GPU between them and the
+    # warm-up: after even 4 ms idle an 8192^3 launch takes 2.4-2.6 ms (2.5-3.2
+    # after 40 ms) and settles near 2.2 ms only after some 50-100 ms of
+    # back-to-back work.
     stats = step_stats(run, args.steps, stream)
     for i in range(args.warmup):
         run(i)
@@ -815,10 +824,10 @@ def main():
                                    "against the first" if n_cmp == args.steps
                                    else "whole output of the last %d timed launches (one buffer "
                                    "each, reused in turn) against each other" % n_cmp)},
-        "step_stats": stats,
+        "step_stats": stats(),
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "comparison": comparison,
+        "comparison": native(),
         "build_id": heal.build_id(),
         "wall_s": round(wall, 3),
     }
