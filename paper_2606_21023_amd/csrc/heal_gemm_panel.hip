@@ -191,8 +191,8 @@ __global__ void __launch_bounds__(PNT, PBM <= 128 ? 2 : 1) gemm_panel_kernel(Pan
         pa[u] = bload(ra, ok ? (uint32_t)((r * p.lda) * ES + c * 16) : kOOB);
     }
 
-    // B fragment of lane (fr, fg), column block j, chunk c: column
-    // n0 + 32 wave + 16 j + fr, k = 32 c + 8 fg .. + 7
+    // B fragment of lane (fr, fg) at step s, column block j, chunk c:
+    // column 128 s + 32 wave + 16 j + fr, k = 32 c + 8 fg .. + 7
     const int64_t all_steps = (N + PBN - 1) / PBN;
     const int s_begin = (int)(all_steps * cs / p.csplit);
     const int s_end = (int)(all_steps * (cs + 1) / p.csplit);
