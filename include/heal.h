@@ -137,7 +137,14 @@ typedef enum heal_instance_t {
                                   products take 256 x 224 where that needs fewer
                                   rounds of workgroups; INT16 scores 128 x 256),
                                   compute-bound shapes */
-    HEAL_INSTANCE_MEDIUM = 2,  /* 128 x 128 output tiles */
+    HEAL_INSTANCE_MEDIUM = 2,  /* 128 x 128 output tiles.  On this and the large
+                                  instance, products with B stored N x K and
+                                  K <= 128 (attention scores: bf16x3 with
+                                  trans_b = 1, and the INT16 scores) whose rows
+                                  are 16-byte aligned run a panel kernel instead:
+                                  a 256-row (bf16x3) or 128-row (INT16) panel of
+                                  A stays in LDS while the workgroup walks the
+                                  columns of C (at least one panel of rows) */
     HEAL_INSTANCE_SKINNY = 3,  /* M <= 64: decode and lm_head shapes, B streamed */
     HEAL_INSTANCE_COUNT = 4
 } heal_instance_t;
