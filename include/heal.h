@@ -34,7 +34,11 @@
  *     not overlap A or B (A and B may alias each other);
  *   - any 4-byte-aligned pointer and any leading dimension are accepted; the
  *     widest loads are used when alignment allows, and the result bits never
- *     depend on which load path ran.
+ *     depend on which load path ran;
+ *   - a product whose output holds more than 2^21 blocks of 16 x 16 elements
+ *     (over all its batch entries) is enqueued as several kernel launches,
+ *     each on a range of batch entries, rows and columns, because a dispatch
+ *     counts its work-items in 32 bits; the bits are those of one launch.
  * Errors: arguments are validated before any HIP call, so an invalid call
  * returns HEAL_ERR_INVALID_VALUE without touching the device.  The library
  * never aborts and never prints.

@@ -36,6 +36,37 @@ bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0
 // M x N outputs whose element count (and so every tile count) fits in 2^62.
 bool product_fits(int64_t M, int64_t N) { return M == 0 || N <= ((int64_t)1 << 62) / M; }
 
+// A dispatch counts work-items in 32 bits per grid dimension.  Every kernel
+// here has at most 1024 threads per workgroup and at most one workgroup per
+// 16 x 16 block of C (the short-K panel kernel also lays its batch entries
+// along the grid), so a launch is held to 2^21 such blocks over its batch
+// entries: at most 2^31 work-items.  Larger calls run as several launches,
+// each on a range of batch entries, rows and columns of C (rows and columns
+// in multiples of 256).  Each output element is summed in the same K order
+// by every kernel, so the result bits do not depend on how a call is cut.
+constexpr int64_t kLaunchBlocks = (int64_t)1 << 21;
+constexpr int64_t kLaunchCols = (int64_t)1 << 20;
+
+template <class F>
+heal_status_t for_each_part(int64_t batch, int64_t M, int64_t N, F launch)
+{
+    auto blocks = [](int64_t x) { return (x + 15) / 16; };
+    const int64_t nc = N < kLaunchCols ? N : kLaunchCols;
+    int64_t mc = kLaunchBlocks / blocks(nc) * 16;   // at least 512 rows
+    mc = mc >= M ? M : mc / 256 * 256;
+    int64_t bc = kLaunchBlocks / (blocks(mc) * blocks(nc));
+    bc = bc < 1 ? 1 : bc > batch ? batch : bc;
+    for (int64_t b0 = 0; b0 < batch; b0 += bc)
+        for (int64_t m0 = 0; m0 < M; m0 += mc)
+            for (int64_t n0 = 0; n0 < N; n0 += nc) {
+                const int64_t bn = batch - b0 < bc ? batch - b0 : bc;
+                const int64_t mn = M - m0 < mc ? M - m0 : mc;
+                const int64_t nn = N - n0 < nc ? N - n0 : nc;
+                if (launch(b0, bn, m0, mn, n0, nn) != hipSuccess) return HEAL_ERR_LAUNCH;
+            }
+    return HEAL_OK;
+}
+
 int select_instance(int64_t M, int64_t N)
 {
     (void)N;
@@ -78,31 +109,34 @@ heal_status_t run_gemm(int instance, int64_t M, int64_t N, int64_t K, float alph
     if (M == 0 || N == 0 || batch == 0) return HEAL_OK;
     st = check_device();
     if (st != HEAL_OK) return st;
-    if (instance == HEAL_INSTANCE_AUTO) instance = select_instance(M, N);
 
     heal::GemmArgs a;
-    a.M = M;
-    a.N = N;
     a.K = K;
-    a.A = A;
     a.lda = lda;
     a.strideA = strideA;
-    a.B = B;
     a.ldb = ldb;
     a.strideB = strideB;
-    a.C = C;
     a.ldc = ldc;
     a.strideC = strideC;
-    a.batch = batch;
     a.alpha = alpha;
     // 16-byte paths need every row start aligned: base pointer, leading
-    // dimension and batch stride all multiples of 4 elements.
+    // dimension and batch stride all multiples of 4 elements (the parts of
+    // a cut call start at multiples of 256 rows and columns).
     a.vecA = aligned16(A) && lda % 4 == 0 && (batch == 1 || strideA % 4 == 0);
     a.vecB = aligned16(B) && ldb % 4 == 0 && (batch == 1 || strideB % 4 == 0);
     a.vecC = aligned16(C) && ldc % 4 == 0 && (batch == 1 || strideC % 4 == 0);
     const bool use_alpha = alpha != 1.0f;
-    hipError_t e = heal::launch_gemm(instance, a, trans_b != 0, use_alpha, stream);
-    return e == hipSuccess ? HEAL_OK : HEAL_ERR_LAUNCH;
+    return for_each_part(batch, M, N, [&](int64_t b0, int64_t bn, int64_t m0, int64_t mn,
+                                         int64_t n0, int64_t nn) {
+        a.M = mn;
+        a.N = nn;
+        a.batch = bn;
+        a.A = A ? A + b0 * strideA + m0 * lda : A;   // null only when K == 0
+        a.B = B ? B + b0 * strideB + (trans_b ? n0 * ldb : n0) : B;
+        a.C = C + b0 * strideC + m0 * ldc + n0;
+        const int inst = instance == HEAL_INSTANCE_AUTO ? select_instance(mn, nn) : instance;
+        return heal::launch_gemm(inst, a, trans_b != 0, use_alpha, stream);
+    });
 }
 
 // Packed operands: K bounded so that every byte offset inside one tile of
@@ -128,20 +162,26 @@ heal_status_t run_packed(int op, int instance, int64_t M, int64_t N, int64_t K, 
     heal_status_t st = check_device();
     if (st != HEAL_OK) return st;
     heal::OpArgs a = {};
-    a.M = M;
-    a.N = N;
     a.K = K;
-    a.A = A;
     a.lda = lda;
-    a.B = Bp;
-    a.C = C;
     a.ldc = ldc;
     a.batch = 1;
     a.e = e;
     a.alpha = 1.0f;
     a.vecA = aligned16(A) && lda % 4 == 0;
     a.vecC = aligned16(C) && ldc % 4 == 0;
-    return heal::launch_gemm_op(op, instance, a, stream) == hipSuccess ? HEAL_OK : HEAL_ERR_LAUNCH;
+    // packed B: a part starting at column n0 (a multiple of 16) starts at
+    // column block n0 / 16, ceil(K/32) chunks of planes x 512 values each
+    const int64_t block_vals = ((K + 31) / 32) * (op == heal::OP_PRESPLIT ? 2 : 1) * 512;
+    return for_each_part(1, M, N, [&](int64_t, int64_t, int64_t m0, int64_t mn, int64_t n0,
+                                      int64_t nn) {
+        a.M = mn;
+        a.N = nn;
+        a.A = A ? A + m0 * lda : A;   // null only when K == 0
+        a.B = Bp ? Bp + (n0 / 16) * block_vals : Bp;
+        a.C = C + m0 * ldc + n0;
+        return heal::launch_gemm_op(op, instance, a, stream);
+    });
 }
 
 }  // namespace
@@ -360,28 +400,29 @@ heal_status_t heal_scores_i16(int64_t M, int64_t N, int64_t K, const int16_t *Q,
     heal_status_t st = check_device();
     if (st != HEAL_OK) return st;
     heal::OpArgs a = {};
-    a.M = M;
-    a.N = N;
     a.K = K;
-    a.A = Q;
     a.lda = ldq;
     a.strideA = strideQ;
-    a.B = Kt;
     a.ldb = ldk;
     a.strideB = strideK;
-    a.C = S;
     a.ldc = lds;
     a.strideC = strideS;
-    a.batch = batch;
     a.maxA = maxQ;
     a.maxB = maxK;
     a.alpha = alpha;
     a.vecA = aligned16(Q) && ldq % 8 == 0 && (batch == 1 || strideQ % 8 == 0);
     a.vecB = aligned16(Kt) && ldk % 8 == 0 && (batch == 1 || strideK % 8 == 0);
     a.vecC = aligned16(S) && lds % 4 == 0 && (batch == 1 || strideS % 4 == 0);
-    return heal::launch_gemm_op(heal::OP_SCORES, HEAL_INSTANCE_AUTO, a, stream) == hipSuccess
-               ? HEAL_OK
-               : HEAL_ERR_LAUNCH;
+    return for_each_part(batch, M, N, [&](int64_t b0, int64_t bn, int64_t m0, int64_t mn,
+                                          int64_t n0, int64_t nn) {
+        a.M = mn;
+        a.N = nn;
+        a.batch = bn;
+        a.A = Q ? Q + b0 * strideQ + m0 * ldq : Q;   // null only when K == 0
+        a.B = Kt ? Kt + b0 * strideK + n0 * ldk : Kt;
+        a.C = S + b0 * strideS + m0 * lds + n0;
+        return heal::launch_gemm_op(heal::OP_SCORES, HEAL_INSTANCE_AUTO, a, stream);
+    });
 }
 
 }  // extern "C"
