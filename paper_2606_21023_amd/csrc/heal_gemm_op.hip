@@ -1272,9 +1272,42 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 #ifndef HEAL_OP_NARROW64_CFG
 #define HEAL_OP_NARROW64_CFG 64, 16, 64, 16, 1024, 64, 2
 #endif
-// 256-column tiles are used while they number at least this many
-#ifndef HEAL_OP_WIDE_MIN_TILES
-#define HEAL_OP_WIDE_MIN_TILES 384
+// M <= 64, outputs between: 32-, 64- and 128-column tiles of 16-column
+// compute waves (32-column ones for 128) and as many waves again that load
+// and convert.  The tile width follows the bf16x3 skinny kernel's strips
+// (the widest that still gives about one tile per CU at 64 rows, two at 16
+// or 32 rows).  On 64 x 16032 x 4096 (one eighth of lm_head's columns)
+// 64-column tiles of 512 threads ran HEAL-Full in 44.6 us, HEAL-Base in
+// 34.8 us and the pre-split product in 54.5 us, against 116.8, 92.9 and
+// 132.1 us for the streamed 16-column tiles (1002 of them, each
+// converting all of A), 48.7 / 36.3 / 61.4 us with 256 threads and
+// 64.4 / 44.8 / 90.4 us for 128-column tiles.
+#ifndef HEAL_OP_MID32_16
+#define HEAL_OP_MID32_16 16, 32, 16, 16, 256, 128, 2
+#endif
+#ifndef HEAL_OP_MID64_16
+#define HEAL_OP_MID64_16 16, 64, 16, 16, 512, 128, 2
+#endif
+#ifndef HEAL_OP_MID128_16
+#define HEAL_OP_MID128_16 16, 128, 16, 32, 512, 64, 2
+#endif
+#ifndef HEAL_OP_MID32_32
+#define HEAL_OP_MID32_32 32, 32, 32, 16, 256, 128, 2
+#endif
+#ifndef HEAL_OP_MID64_32
+#define HEAL_OP_MID64_32 32, 64, 32, 16, 512, 128, 2
+#endif
+#ifndef HEAL_OP_MID128_32
+#define HEAL_OP_MID128_32 32, 128, 32, 32, 512, 64, 2
+#endif
+#ifndef HEAL_OP_MID32_64
+#define HEAL_OP_MID32_64 64, 32, 64, 16, 256, 64, 2
+#endif
+#ifndef HEAL_OP_MID64_64
+#define HEAL_OP_MID64_64 64, 64, 64, 16, 512, 64, 2
+#endif
+#ifndef HEAL_OP_MID128_64
+#define HEAL_OP_MID128_64 64, 128, 64, 32, 512, 64, 2
 #endif
 
 // The same with 224-column tiles (eight waves of 64 x 112), for shapes whose
@@ -1358,7 +1391,21 @@ hipError_t launch_op(int instance, const OpArgs &a, hipStream_t stream)
     case HEAL_INSTANCE_LARGE: return launch_large<OP>(a, stream);
     case HEAL_INSTANCE_MEDIUM: return launch_cfg<OP, HEAL_OP_MEDIUM_CFG>(a, stream);
     case HEAL_INSTANCE_SKINNY: {
-        const bool wide = (a.N + 255) / 256 >= HEAL_OP_WIDE_MIN_TILES;
+        const int w = skinny_strip_width(a.N, a.M);
+        const bool wide = w == 256;
+        if (w == 32 || w == 64 || w == 128) {
+            if (a.M <= 16)
+                return w == 32   ? launch_cfg<OP, HEAL_OP_MID32_16>(a, stream)
+                       : w == 64 ? launch_cfg<OP, HEAL_OP_MID64_16>(a, stream)
+                                 : launch_cfg<OP, HEAL_OP_MID128_16>(a, stream);
+            if (a.M <= 32)
+                return w == 32   ? launch_cfg<OP, HEAL_OP_MID32_32>(a, stream)
+                       : w == 64 ? launch_cfg<OP, HEAL_OP_MID64_32>(a, stream)
+                                 : launch_cfg<OP, HEAL_OP_MID128_32>(a, stream);
+            return w == 32   ? launch_cfg<OP, HEAL_OP_MID32_64>(a, stream)
+                   : w == 64 ? launch_cfg<OP, HEAL_OP_MID64_64>(a, stream)
+                             : launch_cfg<OP, HEAL_OP_MID128_64>(a, stream);
+        }
         if constexpr (OP != OP_SCORES) {
             if (!wide && HEAL_OP_STREAM) {
                 if (a.M <= 16 && vec_path_applies<OP, 16, 16, HEAL_STREAM16_BK>(a))

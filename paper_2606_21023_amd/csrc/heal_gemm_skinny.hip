@@ -9,9 +9,11 @@
 // Work split.  A workgroup owns a strip of BN = 16*CB columns of C and all
 // of its (at most 64) rows, and walks K in stages of BK.  Each element of B
 // is therefore loaded and split by exactly one workgroup; A (at most 64 x K,
-// resident in L2) is re-read by every workgroup.  Strips are narrow (16
-// columns for 4096-wide outputs) so that every CU streams its own share of
-// B: HBM bandwidth needs all CUs with loads in flight.
+// resident in L2) is re-read by every workgroup.  Strips are as wide as
+// the output allows while every CU still gets one (16 columns for 4096-wide
+// outputs, 256 for a 128256-wide lm_head): HBM bandwidth needs all CUs with
+// loads in flight, and wider strips read longer row pieces of B and fewer
+// copies of A.
 //
 // Pipeline.  A and B are staged in a ring of R register sets: while stage s
 // is multiplied out of LDS, stage s+1 is split into the other LDS buffer and
@@ -444,20 +446,33 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 // apart and stream at ~3.4-3.7 TB/s when each load instruction covers whole
 // pieces (~2.5 TB/s with quarter pieces), 32-column strips at ~5.5 TB/s,
 // 128- and 256-column strips at ~6.8 TB/s when there are enough of them.
-// Outputs of 4096 columns have only 256 16-column strips, one per CU, which
-// still beats 128 wider ones at every row count (32 rows: 27 vs 29 us; 64
-// rows: 38 vs 41 us); wide outputs (lm_head) use 256-column strips.  The
-// stage depth is the smallest that gives every thread whole 16-byte units
-// of A and B at the tile's row count.  Narrow strips of 64 rows run 512
-// threads (half blocks of B; 33.6 vs 37.6 us with 256), of 17 to 32 rows
-// 256 threads (25.7 vs 26.5 us with 512), of 16 rows either (22.6 us; a
-// read-only kernel of the same B pattern takes 17.5 us, 20.5 us when it
-// also reads A from L2 as every workgroup here does).  Wide strips (lm_head, 64 x 128256 x 4096, with 16, 32
-// or 64 rows): 256 columns everywhere, 512 threads where every thread still
-// gets whole A quads: 0.43 / 0.40 / 0.37 ms against 0.55 / 0.45 / 0.39 ms
-// for the earlier 128-column strips at 16 and 32 rows and 256 threads.
+// Every strip re-reads all of A (from L2), and the K order keeps each
+// output element in one workgroup, so an output takes the widest strips of
+// which it still has enough: about one per CU at 64 rows (at least
+// HEAL_SKINNY_MIN_STRIPS), about two at 16 or 32 rows, whose A is cheaper
+// to re-read (HEAL_SKINNY_MIN_STRIPS_SMALL), but never 16-column strips
+// while 32-column ones still give one per CU.  4096 deep, 64 rows: 4096
+// columns 35.4 us with 256 16-column strips (35.9 with 128 of 32 columns);
+// 8192 columns 38.7 us with 256 of 32 columns (68.0 with 512 of 16, 61.7
+// with 128 of 64); 16032 columns 66.0 us with 251 of 64 columns (127.9 with
+// 1002 of 16, 72.3 with 501 of 32, 93.1 with 126 of 128); 32064 columns
+// 110 us with 251 of 128 (131 with 501 of 64).  16 rows: 8192 columns 28.9
+// us with 256 of 32 (41.6 with 512 of 16); 16032 columns 46.8 us with 501
+// of 32 (53.9 with 251 of 64); 65536 columns 212 us with 512 of 128 (241
+// with 256 of 256).  The stage depth
+// is the smallest that gives every thread whole 16-byte units of A and B at
+// the tile's row count.  16-column strips of 64 rows run 512 threads (half
+// blocks of B; 33.6 vs 37.6 us with 256), of 17 to 32 rows 256 threads
+// (25.7 vs 26.5 us with 512), of 16 rows either (22.6 us; a read-only
+// kernel of the same B pattern takes 17.5 us, 20.5 us when it also reads A
+// from L2 as every workgroup here does).  256-column strips (lm_head, 64 x
+// 128256 x 4096, with 16, 32 or 64 rows): 512 threads where every thread
+// still gets whole A quads: 0.43 / 0.40 / 0.37 ms against 0.55 / 0.45 /
+// 0.39 ms for 128-column strips at 16 and 32 rows and 256 threads.
+// Configurations: CB (16-column blocks per strip), BK, R, NT; the suffix is
+// the strip width, _1 / _2 / _4 the row count (16 / 32 / 64 rows).
 #ifndef HEAL_SKINNY_N1
-#define HEAL_SKINNY_N1 1, 256, 2, 512      // M <= 16, narrow: CB, BK, R, NT
+#define HEAL_SKINNY_N1 1, 256, 2, 512
 #endif
 #ifndef HEAL_SKINNY_N2
 #define HEAL_SKINNY_N2 1, 128, 2, 256
@@ -465,8 +480,29 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 #ifndef HEAL_SKINNY_N4
 #define HEAL_SKINNY_N4 1, 256, 2, 512      // 160 KB of LDS: one workgroup per CU
 #endif
+#ifndef HEAL_SKINNY_S32
+#define HEAL_SKINNY_S32 2, 128, 2, 512     // half blocks of B, every row count
+#endif
+#ifndef HEAL_SKINNY_S64_1
+#define HEAL_SKINNY_S64_1 4, 64, 2, 256
+#endif
+#ifndef HEAL_SKINNY_S64_2
+#define HEAL_SKINNY_S64_2 4, 64, 2, 256
+#endif
+#ifndef HEAL_SKINNY_S64_4
+#define HEAL_SKINNY_S64_4 4, 64, 2, 256
+#endif
+#ifndef HEAL_SKINNY_S128_1
+#define HEAL_SKINNY_S128_1 8, 64, 2, 256
+#endif
+#ifndef HEAL_SKINNY_S128_2
+#define HEAL_SKINNY_S128_2 8, 64, 2, 512
+#endif
+#ifndef HEAL_SKINNY_S128_4
+#define HEAL_SKINNY_S128_4 8, 64, 2, 512
+#endif
 #ifndef HEAL_SKINNY_W1
-#define HEAL_SKINNY_W1 16, 64, 2, 256      // M <= 16, wide (strips of 16*CB columns)
+#define HEAL_SKINNY_W1 16, 64, 2, 256
 #endif
 #ifndef HEAL_SKINNY_W2
 #define HEAL_SKINNY_W2 16, 64, 2, 512
@@ -474,26 +510,49 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 #ifndef HEAL_SKINNY_W4
 #define HEAL_SKINNY_W4 16, 32, 2, 512
 #endif
-#ifndef HEAL_SKINNY_WIDE_MIN_N
-#define HEAL_SKINNY_WIDE_MIN_N 16384
+#ifndef HEAL_SKINNY_MIN_STRIPS
+#define HEAL_SKINNY_MIN_STRIPS 240
+#endif
+#ifndef HEAL_SKINNY_MIN_STRIPS_SMALL
+#define HEAL_SKINNY_MIN_STRIPS_SMALL 480
 #endif
 
 template <int MB>
 hipError_t launch_shape(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
 {
-    const bool wide = a.N >= HEAL_SKINNY_WIDE_MIN_N;
-    if constexpr (MB == 1)
-        return wide ? launch_mb<1, HEAL_SKINNY_W1>(a, trans_b, use_alpha, stream)
-                    : launch_mb<1, HEAL_SKINNY_N1>(a, trans_b, use_alpha, stream);
-    else if constexpr (MB == 2)
-        return wide ? launch_mb<2, HEAL_SKINNY_W2>(a, trans_b, use_alpha, stream)
-                    : launch_mb<2, HEAL_SKINNY_N2>(a, trans_b, use_alpha, stream);
-    else
-        return wide ? launch_mb<4, HEAL_SKINNY_W4>(a, trans_b, use_alpha, stream)
-                    : launch_mb<4, HEAL_SKINNY_N4>(a, trans_b, use_alpha, stream);
+    const int w = skinny_strip_width(a.N, a.M);
+    if (w == 32) return launch_mb<MB, HEAL_SKINNY_S32>(a, trans_b, use_alpha, stream);
+    if constexpr (MB == 1) {
+        if (w == 256) return launch_mb<1, HEAL_SKINNY_W1>(a, trans_b, use_alpha, stream);
+        if (w == 128) return launch_mb<1, HEAL_SKINNY_S128_1>(a, trans_b, use_alpha, stream);
+        if (w == 64) return launch_mb<1, HEAL_SKINNY_S64_1>(a, trans_b, use_alpha, stream);
+        return launch_mb<1, HEAL_SKINNY_N1>(a, trans_b, use_alpha, stream);
+    } else if constexpr (MB == 2) {
+        if (w == 256) return launch_mb<2, HEAL_SKINNY_W2>(a, trans_b, use_alpha, stream);
+        if (w == 128) return launch_mb<2, HEAL_SKINNY_S128_2>(a, trans_b, use_alpha, stream);
+        if (w == 64) return launch_mb<2, HEAL_SKINNY_S64_2>(a, trans_b, use_alpha, stream);
+        return launch_mb<2, HEAL_SKINNY_N2>(a, trans_b, use_alpha, stream);
+    } else {
+        if (w == 256) return launch_mb<4, HEAL_SKINNY_W4>(a, trans_b, use_alpha, stream);
+        if (w == 128) return launch_mb<4, HEAL_SKINNY_S128_4>(a, trans_b, use_alpha, stream);
+        if (w == 64) return launch_mb<4, HEAL_SKINNY_S64_4>(a, trans_b, use_alpha, stream);
+        return launch_mb<4, HEAL_SKINNY_N4>(a, trans_b, use_alpha, stream);
+    }
 }
 
 }  // namespace
+
+// Strip width in columns for an output of N columns and M <= 64 rows: the
+// widest of 256, 128, 64 and 32 with at least HEAL_SKINNY_MIN_STRIPS_SMALL
+// strips at up to 32 rows (HEAL_SKINNY_MIN_STRIPS above), else 32 if that
+// still gives HEAL_SKINNY_MIN_STRIPS, else 16.
+int skinny_strip_width(int64_t N, int64_t M)
+{
+    const int64_t least = M <= 32 ? HEAL_SKINNY_MIN_STRIPS_SMALL : HEAL_SKINNY_MIN_STRIPS;
+    for (int w = 256; w >= 32; w /= 2)
+        if ((N + w - 1) / w >= least) return w;
+    return (N + 31) / 32 >= HEAL_SKINNY_MIN_STRIPS ? 32 : 16;
+}
 
 bool skinny_kernel_applies(const GemmArgs &a, bool trans_b)
 {

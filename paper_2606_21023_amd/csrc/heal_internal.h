@@ -34,6 +34,9 @@ hipError_t launch_gemm_large(const GemmArgs &args, bool trans_b, bool use_alpha,
                              hipStream_t stream);
 
 // The skinny kernel (heal_gemm_skinny.hip): M <= 64, 16-byte operand rows.
+// skinny_strip_width: the column-strip width (16, 32, 64, 128 or 256) that
+// an M x N output with M <= 64 takes, shared by every skinny product.
+int skinny_strip_width(int64_t N, int64_t M);
 bool skinny_kernel_applies(const GemmArgs &args, bool trans_b);
 hipError_t launch_gemm_skinny(const GemmArgs &args, bool trans_b, bool use_alpha,
                               hipStream_t stream);

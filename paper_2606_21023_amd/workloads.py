@@ -69,6 +69,14 @@ WORKLOADS = {
                            note="M=N=K=8192, A,B ~ N(0,1)"),
     "lm_head": Workload("lm_head", 64, 128256, 4096, seed=5, sigma_b=0.02,
                         note="lm_head 64x4096 @ 4096x128256"),
+    # one GPU's column shard of a layer split 8 ways by N (tensor parallel:
+    # B sliced by columns, A replicated)
+    "lm_head_tp8": Workload("lm_head_tp8", 64, 16032, 4096, seed=6, sigma_b=0.02,
+                            note="lm_head column shard 64x4096 @ 4096x16032 (1/8 of 128256)"),
+    "prefill_up_tp8": Workload("prefill_up_tp8", 2048, 1792, 4096, seed=7, sigma_b=0.02,
+                               outlier_frac=0.001,
+                               note="prefill up-projection column shard 2048x4096 @ 4096x1792 "
+                                    "(1/8 of 14336)"),
 }
 
 

@@ -462,8 +462,10 @@ def factor(orc, mq, mk, alpha):
     return orc.scores_factor(mq, mk, alpha)
 
 
+# the last two: at most 64 rows and 8196 or 16004 columns, on 32- and
+# 64-column tiles
 SCORE_SHAPES = [(1, 1, 1, 1), (1, 17, 31, 33), (2, 64, 70, 128), (3, 129, 257, 64),
-                (1, 300, 200, 136)]
+                (1, 300, 200, 136), (2, 16, 8196, 40), (1, 33, 16004, 64)]
 
 
 @pytest.mark.parametrize("shape", SCORE_SHAPES, ids=lambda s: "x".join(map(str, s)))
@@ -617,6 +619,43 @@ def test_stream_tiles_every_m_bitwise(orc, N, K):
     announce("stream tiles every M, pre-split N=%d K=%d" % (N, K))
     ref = heal.heal_gemm_f32_presplit(Ad, Bp, N, instance=heal.INSTANCE_MEDIUM)
     torch.cuda.synchronize()
+    for m in range(1, 65):
+        C = heal.heal_gemm_f32_presplit(Ad[:m], Bp, N, instance=heal.INSTANCE_SKINNY)
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "pre-split M=%d" % m
+
+
+@pytest.mark.parametrize("N,K", [(8196, 100), (16004, 68), (30724, 36)],
+                         ids=["w32", "w32-w64", "w64-w128"])
+def test_mid_width_tiles_every_m_bitwise(orc, N, K):
+    """Every row count 1..64 through the skinny instance of the packed-weight
+    products where the output is too wide for the streamed 16-column tiles
+    and too narrow for 256-column ones: 32-, 64- and 128-column tiles (by
+    row count as noted in the ids), ragged last tile, K tail.  Each row
+    bitwise equal to the medium instance's, whose 64-row result is checked
+    against the oracle."""
+    A = wl.random_matrix((64, K), seed=2 * N + K, sigma=2.0)
+    W = wl.random_matrix((N, K), seed=N + 7 * K, sigma=0.02)
+    e = heal.heal_f16_weight_exponent(float(np.abs(W).max()))
+    Ad, Wd = to_dev(A), to_dev(W)
+    W16 = heal.heal_pack_f16_weight(Wd, e)
+    Bp = heal.heal_presplit_b(Wd, trans_b=True)
+    for products in (1, 2):
+        announce("mid-width tiles every M, f16w p%d N=%d K=%d" % (products, N, K))
+        ref = heal.heal_gemm_f16w(Ad, W16, N, e, products, instance=heal.INSTANCE_MEDIUM)
+        torch.cuda.synchronize()
+        _, S = orc.gemm_f16w(A, W, e, products)
+        check_tolerance(ref.cpu().numpy(), S, f16w_absprod(orc, A, W, e), "p%d" % products)
+        for m in range(1, 65):
+            C = heal.heal_gemm_f16w(Ad[:m], W16, N, e, products, instance=heal.INSTANCE_SKINNY)
+            torch.cuda.synchronize()
+            assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), \
+                "p%d M=%d differs" % (products, m)
+    announce("mid-width tiles every M, pre-split N=%d K=%d" % (N, K))
+    ref = heal.heal_gemm_f32_presplit(Ad, Bp, N, instance=heal.INSTANCE_MEDIUM)
+    C3 = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Wd.t().contiguous())
+    torch.cuda.synchronize()
+    assert torch.equal(ref.view(torch.int32), C3.view(torch.int32)), "pre-split differs from bf16x3"
     for m in range(1, 65):
         C = heal.heal_gemm_f32_presplit(Ad[:m], Bp, N, instance=heal.INSTANCE_SKINNY)
         torch.cuda.synchronize()

@@ -264,13 +264,22 @@ def test_instances_bitwise_equal(shape):
             "%s differs from large" % INAME[inst]
 
 
-@pytest.mark.parametrize("N,K", [(1040, 1028), (300, 520), (16400, 260)],
-                         ids=["narrow-ktail", "narrow-ragged-n", "wide"])
+# output widths and the strips the skinny kernel takes for them (the widest
+# that still gives about one strip per CU at 64 rows, two at 16 or 32 rows),
+# each with a ragged last strip and a K tail: 16 columns; 16; 32; 32 at up
+# to 32 rows, else 64; 64, else 128; 128, else 256; 256 at every row count
+SKINNY_WIDTHS = [(1040, 1028), (300, 520), (8196, 100), (16004, 68), (30724, 36), (61444, 36),
+                 (122884, 12)]
+SKINNY_WIDTH_IDS = ["s16-ktail", "s16-ragged-n", "s32", "s32-s64", "s64-s128", "s128-s256",
+                    "s256"]
+
+
+@pytest.mark.parametrize("N,K", SKINNY_WIDTHS, ids=SKINNY_WIDTH_IDS)
 def test_skinny_every_m_bitwise(N, K):
     """Every row count 1..64 through the skinny instance (16-row, 32-row and
-    64-row tiles; narrow strips with the row-contiguous B map, and wide
-    strips), B stored K x N with a K tail and a ragged last strip: each row
-    bitwise equal to the medium instance's row of the full 64-row product."""
+    64-row tiles; strips of 16 to 256 columns), B stored K x N with a K tail
+    and a ragged last strip: each row bitwise equal to the medium instance's
+    row of the full 64-row product."""
     A = wl.random_matrix((64, K), seed=N + K)
     B = wl.random_matrix((K, N), seed=N + 2 * K)
     Ad, Bd = to_dev(A), to_dev(B)
@@ -281,6 +290,30 @@ def test_skinny_every_m_bitwise(N, K):
         C = heal.heal_gemm_f32_instance(heal.INSTANCE_SKINNY, Ad[:m], Bd)
         torch.cuda.synchronize()
         assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "M=%d differs" % m
+
+
+@pytest.mark.parametrize("N,K", SKINNY_WIDTHS[2:], ids=SKINNY_WIDTH_IDS[2:])
+def test_skinny_widths_trans_b_alpha(orc, N, K):
+    """The wider strips with B stored N x K and alpha, at the row counts
+    around the 16-, 32- and 64-row tiles: bitwise equal to the medium
+    instance, and the 33-row product element by element against the oracle."""
+    A = wl.random_matrix((64, K), seed=3 * N + K)
+    Bt = wl.random_matrix((N, K), seed=N + 5 * K)
+    alpha = 0.375
+    Ad, Bd = to_dev(A)[None], to_dev(Bt)[None]
+    announce("skinny widths trans_b %dx%d" % (N, K))
+    ref = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Bd, alpha=alpha, trans_b=True)
+    torch.cuda.synchronize()
+    for m in (1, 15, 16, 17, 32, 33, 63, 64):
+        C = heal.heal_gemm_f32_instance(heal.INSTANCE_SKINNY, Ad[:, :m], Bd, alpha=alpha,
+                                        trans_b=True)
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int32), ref[:, :m].view(torch.int32)), "M=%d differs" % m
+        if m == 33:
+            B = np.ascontiguousarray(Bt.T)
+            _, S = orc.gemm3(A[:m], B)
+            check_tolerance(C[0].cpu().numpy(), alpha * S, alpha * abs_product(A[:m], B),
+                            "skinny %d columns trans_b" % N)
 
 
 @pytest.mark.parametrize("K", [8, 7], ids=["k8", "k7"])
