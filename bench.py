@@ -81,8 +81,20 @@ KERNEL_SOURCES = {1: ["heal_gemm_large.hip", "heal_device.h", "heal_internal.h"]
                   "op": ["heal_gemm_op.hip", "heal_device.h", "heal_internal.h"],
                   "panel": ["heal_gemm_panel.hip", "heal_device.h", "heal_internal.h"],
                   "split": ["heal_split.hip", "heal_device.h", "heal_internal.h"]}
-OP_INSTANCE_NAMES = {1: "large 128x256, 8 waves", 2: "medium 128x128, 8 waves",
+OP_INSTANCE_NAMES = {1: "large 128x256, 8 waves", 2: "medium 128x128, 8 waves, two register sets",
                      3: "skinny M<=64, 256-column tiles"}
+
+
+def skinny_strip_width(N, M):
+    """Column-strip width of an M x N output with M <= 64, as the library
+    picks it (skinny_strip_width in heal_gemm_skinny.hip): the widest of 256,
+    128, 64 and 32 columns with at least 480 strips at up to 32 rows (240
+    above), else 32 if that still gives 240 strips, else 16."""
+    least = 480 if M <= 32 else 240
+    for w in (256, 128, 64, 32):
+        if -(-N // w) >= least:
+            return w
+    return 32 if -(-N // 32) >= 240 else 16
 # MFMA products per 32-deep chunk and output block, and bytes per operand element
 METHODS = {
     "bf16x3": {"products": 3, "a_bytes": 4, "b_bytes": 4, "dtype": "bf16x3-f32acc"},
@@ -747,13 +759,18 @@ def main():
     elif method == "bf16x3":
         traffic = measured_traffic(w.name, instance)
         kernel = KERNEL_NAMES.get(instance, "?")
+        if instance == 3:
+            kernel = "gemm_skinny_kernel (%d-column strips, M <= 64)" % skinny_strip_width(w.N, w.M)
     else:
         traffic = measured_traffic("%s:%s" % (method, w.name), "op")
         label = OP_INSTANCE_NAMES.get(instance, "?")
         kname = "gemm_op_kernel"
-        if instance == 3 and method != "i16_scores" and -(-w.N // 256) < 384:
-            # M <= 64 with fewer than 384 256-column tiles: the streamed
-            # narrow tiles (loader waves and one computing wave, 16 columns)
+        sw = skinny_strip_width(w.N, w.M) if instance == 3 else 0
+        if instance == 3 and sw in (32, 64, 128):
+            label = "skinny M<=64, %d-column tiles, loader waves beside the MFMA waves" % sw
+        elif instance == 3 and method != "i16_scores" and sw == 16:
+            # M <= 64 with too few wider tiles: the streamed narrow tiles
+            # (loader waves and one computing wave, 16 columns)
             kname = "gemm_op_stream_kernel"
             label = "narrow 16-column tiles, loader waves + one MFMA wave, LDS ring"
         elif instance == 1 and method != "i16_scores":

@@ -1244,8 +1244,13 @@ hipError_t launch_cfg(const OpArgs &a, hipStream_t stream)
 #ifndef HEAL_OP_LARGE_PRESPLIT_CFG
 #define HEAL_OP_LARGE_PRESPLIT_CFG 256, 256, 64, 128, 512, 32
 #endif
+// Medium tiles keep two register sets: each stage's loads have a whole
+// stage to arrive (at 4096 deep on 2048 x 1792, 1024 x 1024, 2048 x 2048
+// and 512 x 4096 outputs: HEAL-Full 1.16-1.55x, HEAL-Base 1.7-1.9x, the
+// pre-split product 1.23-1.33x faster than one set; 64-deep stages with
+// two sets were within 10% either way).
 #ifndef HEAL_OP_MEDIUM_CFG
-#define HEAL_OP_MEDIUM_CFG 128, 128, 32, 64, 512, 32
+#define HEAL_OP_MEDIUM_CFG 128, 128, 32, 64, 512, 32, 2
 #endif
 // M <= 64, wide N: 256-column tiles, four compute waves of 16..64 x 64
 #ifndef HEAL_OP_SKINNY16_CFG

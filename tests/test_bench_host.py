@@ -104,3 +104,20 @@ def test_profile_summary_averages_the_timed_dispatches(tmp_path):
     assert "timed dispatches' trace average: 0.5000" in text
     # FETCH x2 (524288 KiB per 1 GiB copy), WRITE x1: 100 KiB * 2 + 50 KiB
     assert "Traffic %.4g bytes" % (100 * 1024 * 2.0 + 50 * 1024) in text
+
+
+def test_strip_width_rule_matches_the_library():
+    """bench.py labels skinny kernels with the strip width the library picks;
+    its copy of the rule uses the thresholds heal_gemm_skinny.hip defines."""
+    import re
+    with open(os.path.join(ROOT, "paper_2606_21023_amd", "csrc", "heal_gemm_skinny.hip")) as f:
+        src = f.read()
+    big = int(re.search(r"#define HEAL_SKINNY_MIN_STRIPS (\d+)", src).group(1))
+    small = int(re.search(r"#define HEAL_SKINNY_MIN_STRIPS_SMALL (\d+)", src).group(1))
+    assert (big, small) == (240, 480)
+    sw = bench.skinny_strip_width
+    assert [sw(4096, m) for m in (1, 16, 17, 64)] == [16, 16, 16, 16]
+    assert [sw(8192, m) for m in (16, 64)] == [32, 32]
+    assert [sw(16032, m) for m in (16, 32, 33, 64)] == [32, 32, 64, 64]
+    assert [sw(65536, m) for m in (16, 64)] == [128, 256]
+    assert [sw(122625, 16), sw(122624, 16), sw(128256, 64)] == [256, 128, 256]
