@@ -22,6 +22,8 @@
 // 16 output columns n) and the A fragment the second (16 columns = output
 // rows m), so each lane's four accumulators are C[m][n..n+3], four
 // consecutive FP32 of one output row, written with one 16-byte store.
+#include <type_traits>
+
 #include "heal.h"
 #include "heal_device.h"
 #include "heal_internal.h"
@@ -45,12 +47,23 @@ constexpr int kChunk = 32;  // K depth of one bf16 MFMA: the unit of the reducti
 #ifndef HEAL_SCHED_SPLIT_AT
 #define HEAL_SCHED_SPLIT_AT 4
 #endif
-// Instance configurations: BM, BN, BK, WM, WN, threads.  The medium tile
-// stages 64-deep: two MFMA chunks per barrier and per round of loads (at
-// 4096 deep 1.30-1.34x faster than 32-deep stages on 2048 x 1792, 2048 x
-// 2048, 1024 x 1024 and 512 x 4096 outputs; 1.02-1.05x at 256 deep).
+// The same with the register ring (loads two stages ahead), and the fewest
+// full stages for which the ring runs: on 4096-deep medium tiles the ring
+// with the split from 2/8 of the stage was 1.17-1.32x faster than one set
+// (4/8: 1.10-1.27x); on 256-deep ones (4 stages) it was 4-7% slower.
+#ifndef HEAL_SCHED_SPLIT_AT_RING
+#define HEAL_SCHED_SPLIT_AT_RING 2
+#endif
+#ifndef HEAL_RING_MIN_STAGES
+#define HEAL_RING_MIN_STAGES 8
+#endif
+// Instance configurations: BM, BN, BK, WM, WN, threads[, register sets].
+// The medium tile stages 64-deep: two MFMA chunks per barrier and per round
+// of loads (at 4096 deep 1.30-1.34x faster than 32-deep stages on 2048 x
+// 1792, 2048 x 2048, 1024 x 1024 and 512 x 4096 outputs; 1.02-1.05x at 256
+// deep).
 #ifndef HEAL_MEDIUM_CFG
-#define HEAL_MEDIUM_CFG 128, 128, 64, 32, 64, 512
+#define HEAL_MEDIUM_CFG 128, 128, 64, 32, 64, 512, 2
 #endif
 #ifndef HEAL_SKINNY16_CFG
 #define HEAL_SKINNY16_CFG 16, 64, 64, 16, 16, 256
@@ -136,11 +149,16 @@ __device__ __forceinline__ void store_pair(char *plane, int off, uint32_t a, uin
     *reinterpret_cast<u32x2 *>(plane + off) = v;
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int NT, bool TRANS_B, bool ALPHA, bool VEC>
+// RS: register sets of staged operands.  With two (tiles whose waves all
+// multiply), each stage's loads are issued two stages before their split;
+// with one, half a stage before.
+template <int BM, int BN, int BK, int WM, int WN, int NT, int RS, bool TRANS_B, bool ALPHA, bool VEC>
 __global__ void __launch_bounds__(NT)
 gemm_bf16x3_kernel(GemmArgs p)
 {
     using T = Tile<BM, BN, BK, WM, WN, NT>;
+    static_assert(RS == 1 || RS == 2, "register sets");
+    constexpr bool RING = RS == 2 && T::CWAVES * 64 == NT;
     // Work distribution of the loads (see the load lambdas below).
     constexpr int A_ROWS_PER_PASS = NT / T::KQ;          // A rows covered by one pass of NT threads
     constexpr int BT_ROWS_PER_PASS = NT / T::KQ;         // same for B stored N x K
@@ -227,8 +245,8 @@ gemm_bf16x3_kernel(GemmArgs p)
 #pragma unroll
             for (int i = 0; i < WM / 16; ++i) acc[j][i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-        f32x4 ra[T::ITA];
-        f32x4 rb[TRANS_B ? T::ITBT : T::ITB][TRANS_B ? 1 : 4];
+        f32x4 ra[RS][T::ITA];
+        f32x4 rb[RS][TRANS_B ? T::ITBT : T::ITB][TRANS_B ? 1 : 4];
 
         // Full stage of an interior tile: buffer loads, one 32-bit VGPR offset
         // per operand and thread; stage and pass offsets are scalar.
@@ -238,32 +256,34 @@ gemm_bf16x3_kernel(GemmArgs p)
         const int voff_a = (a_row * (int)p.lda + 4 * a_kq) * 4;
         const int voff_b = TRANS_B ? (a_row * (int)p.ldb + 4 * a_kq) * 4
                                    : (4 * b_kq * (int)p.ldb + 4 * b_nq) * 4;
-        auto load_stage_fast = [&](int64_t k0) {
-#pragma unroll
-            for (int it = 0; it < T::ITA; ++it)
-                if (T::QA % NT == 0 || it * NT + tid < T::QA)
-                    ra[it] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                        rsrc_a, voff_a, (int)(k0 * 4) + it * A_ROWS_PER_PASS * (int)p.lda * 4, 0));
+        // One pass `it` of A, or of B, of a full stage into register set `set`.
+        auto load_a_fast = [&](int set, int it, int64_t k0) {
+            if (T::QA % NT == 0 || it * NT + tid < T::QA)
+                ra[set][it] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                    rsrc_a, voff_a, (int)(k0 * 4) + it * A_ROWS_PER_PASS * (int)p.lda * 4, 0));
+        };
+        auto load_b_fast = [&](int set, int it, int64_t k0) {
             if (TRANS_B) {
                 const __amdgpu_buffer_rsrc_t rsrc_b = __builtin_amdgcn_make_buffer_rsrc(
                     const_cast<float *>(B + n0 * p.ldb), (short)0, 0x7fffffff, kRsrcFlags);
-#pragma unroll
-                for (int it = 0; it < T::ITBT; ++it)
-                    if (T::QBT % NT == 0 || it * NT + tid < T::QBT)
-                        rb[it][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                            rsrc_b, voff_b,
-                            (int)(k0 * 4) + it * BT_ROWS_PER_PASS * (int)p.ldb * 4, 0));
+                if (T::QBT % NT == 0 || it * NT + tid < T::QBT)
+                    rb[set][it][0] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                        rsrc_b, voff_b, (int)(k0 * 4) + it * BT_ROWS_PER_PASS * (int)p.ldb * 4, 0));
             } else {
                 const __amdgpu_buffer_rsrc_t rsrc_b = __builtin_amdgcn_make_buffer_rsrc(
                     const_cast<float *>(B + k0 * p.ldb + n0), (short)0, 0x7fffffff, kRsrcFlags);
+                if ((BN / 4) % B_NQ_PER_PASS == 0 || b_nq + it * B_NQ_PER_PASS < BN / 4)
 #pragma unroll
-                for (int it = 0; it < T::ITB; ++it)
-                    if ((BN / 4) % B_NQ_PER_PASS == 0 || b_nq + it * B_NQ_PER_PASS < BN / 4)
-#pragma unroll
-                        for (int kk = 0; kk < 4; ++kk)
-                            rb[it][kk] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                rsrc_b, voff_b, kk * (int)p.ldb * 4 + it * B_NQ_PER_PASS * 16, 0));
+                    for (int kk = 0; kk < 4; ++kk)
+                        rb[set][it][kk] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                            rsrc_b, voff_b, kk * (int)p.ldb * 4 + it * B_NQ_PER_PASS * 16, 0));
             }
+        };
+        auto load_stage_fast = [&](int64_t k0, int set) {
+#pragma unroll
+            for (int it = 0; it < T::ITA; ++it) load_a_fast(set, it, k0);
+#pragma unroll
+            for (int it = 0; it < (TRANS_B ? T::ITBT : T::ITB); ++it) load_b_fast(set, it, k0);
         };
 
         // Any stage: element-wise bounds checks, zero fill outside.
@@ -272,16 +292,16 @@ gemm_bf16x3_kernel(GemmArgs p)
             for (int it = 0; it < T::ITA; ++it)
                 if (T::QA % NT == 0 || it * NT + tid < T::QA) {
                     const int64_t r = it * A_ROWS_PER_PASS;
-                    ra[it] = load_quad_checked<VEC>(pa + r * p.lda + k0, m0 + a_row + r < M,
-                                               k0 + 4 * a_kq, K);
+                    ra[0][it] = load_quad_checked<VEC>(pa + r * p.lda + k0, m0 + a_row + r < M,
+                                                  k0 + 4 * a_kq, K);
                 }
             if (TRANS_B) {
 #pragma unroll
                 for (int it = 0; it < T::ITBT; ++it)
                     if (T::QBT % NT == 0 || it * NT + tid < T::QBT) {
                         const int64_t r = it * BT_ROWS_PER_PASS;
-                        rb[it][0] = load_quad_checked<VEC>(pb + r * p.ldb + k0, n0 + a_row + r < N,
-                                                      k0 + 4 * a_kq, K);
+                        rb[0][it][0] = load_quad_checked<VEC>(pb + r * p.ldb + k0, n0 + a_row + r < N,
+                                                         k0 + 4 * a_kq, K);
                     }
             } else {
 #pragma unroll
@@ -290,7 +310,7 @@ gemm_bf16x3_kernel(GemmArgs p)
 #pragma unroll
                         for (int kk = 0; kk < 4; ++kk) {
                             const int64_t kr = k0 + 4 * b_kq + kk;
-                            rb[it][kk] = load_quad_checked<VEC>(
+                            rb[0][it][kk] = load_quad_checked<VEC>(
                                 pb + (k0 + kk) * p.ldb + 4 * it * B_NQ_PER_PASS, kr < K,
                                 n0 + 4 * (b_nq + it * B_NQ_PER_PASS), N);
                         }
@@ -300,15 +320,15 @@ gemm_bf16x3_kernel(GemmArgs p)
         // Split units: one 4-element quad (two split2 calls, two 8-byte LDS
         // writes per plane pair) of this thread's staged data.
         constexpr int NU = T::ITA + (TRANS_B ? T::ITBT : 4 * T::ITB);
-        auto store_unit = [&](char *s, const int u) {
+        auto store_unit = [&](char *s, const int u, const int set) {
             char *a_hi = s, *a_lo = s + T::A_PLANE;
             char *b_hi = s + 2 * T::A_PLANE, *b_lo = b_hi + T::B_PLANE;
             uint32_t h0, l0, h1, l1;
             if (u < T::ITA) {
                 const int it = u;
                 if (T::QA % NT == 0 || it * NT + tid < T::QA) {
-                    split2(ra[it].x, ra[it].y, h0, l0);
-                    split2(ra[it].z, ra[it].w, h1, l1);
+                    split2(ra[set][it].x, ra[set][it].y, h0, l0);
+                    split2(ra[set][it].z, ra[set][it].w, h1, l1);
                     const int off = a_st + it * A_ROWS_PER_PASS * T::ROWB;
                     store_pair(a_hi, off, h0, h1);
                     store_pair(a_lo, off, l0, l1);
@@ -316,8 +336,8 @@ gemm_bf16x3_kernel(GemmArgs p)
             } else if (TRANS_B) {
                 const int it = u - T::ITA;
                 if (T::QBT % NT == 0 || it * NT + tid < T::QBT) {
-                    split2(rb[it][0].x, rb[it][0].y, h0, l0);
-                    split2(rb[it][0].z, rb[it][0].w, h1, l1);
+                    split2(rb[set][it][0].x, rb[set][it][0].y, h0, l0);
+                    split2(rb[set][it][0].z, rb[set][it][0].w, h1, l1);
                     const int off = bt_st + it * BT_ROWS_PER_PASS * T::ROWB;
                     store_pair(b_hi, off, h0, h1);
                     store_pair(b_lo, off, l0, l1);
@@ -326,8 +346,8 @@ gemm_bf16x3_kernel(GemmArgs p)
                 // register transpose: column nn of the 4x4 block is 4 consecutive k
                 const int it = (u - T::ITA) / 4, nn = (u - T::ITA) % 4;
                 if ((BN / 4) % B_NQ_PER_PASS == 0 || b_nq + it * B_NQ_PER_PASS < BN / 4) {
-                    split2(rb[it][0][nn], rb[it][1][nn], h0, l0);
-                    split2(rb[it][2][nn], rb[it][3][nn], h1, l1);
+                    split2(rb[set][it][0][nn], rb[set][it][1][nn], h0, l0);
+                    split2(rb[set][it][2][nn], rb[set][it][3][nn], h1, l1);
                     const int off = T::quad_off(T::brow(4 * (b_nq + it * B_NQ_PER_PASS) + nn), b_kq);
                     store_pair(b_hi, off, h0, h1);
                     store_pair(b_lo, off, l0, l1);
@@ -335,9 +355,21 @@ gemm_bf16x3_kernel(GemmArgs p)
             }
         };
 
-        auto store_stage = [&](char *s) {
+        auto store_stage = [&](char *s, int set) {
 #pragma unroll
-            for (int u = 0; u < NU; ++u) store_unit(s, u);
+            for (int u = 0; u < NU; ++u) store_unit(s, u, set);
+        };
+        // Ring: reload the registers of unit u of `set` with the stage at
+        // k0 once the unit is split (B stored K x N: a 4x4 block's four rows
+        // after its last column).
+        auto reload_unit = [&](int u, int set, int64_t k0) {
+            if (u < T::ITA) {
+                load_a_fast(set, u, k0);
+            } else if (TRANS_B) {
+                load_b_fast(set, u - T::ITA, k0);
+            } else if ((u - T::ITA) % 4 == 3) {
+                load_b_fast(set, (u - T::ITA) / 4, k0);
+            }
         };
 
         // One steady-state stage of an interior tile, software-interleaved:
@@ -345,12 +377,16 @@ gemm_bf16x3_kernel(GemmArgs p)
         // one 32-deep k step each), and the split of the next stage's data is
         // spread over the later chunks, so that VALU work issues while the
         // matrix cores run.  Scheduling barriers keep the chunks apart.
-        auto stage_fast = [&](const char *cur, char *nxt, int64_t k_next) {
-            load_stage_fast(k_next);
+        // k_next: with one register set, the stage loaded now and split into
+        // `nxt` later in this stage; with the ring, the stage that reloads
+        // `set` after its split (set holds the stage split into `nxt`).
+        auto stage_fast = [&](const char *cur, char *nxt, int set, int64_t k_next, auto ring_tag) {
+            constexpr bool R2 = decltype(ring_tag)::value;
+            if (!R2) load_stage_fast(k_next, 0);
             const char *a_hi = cur, *a_lo = cur + T::A_PLANE;
             const char *b_hi = cur + 2 * T::A_PLANE, *b_lo = b_hi + T::B_PLANE;
             constexpr int NJ = WN / 16, KS = BK / kChunk, NC = NJ * KS;
-            constexpr int C0s = NC * HEAL_SCHED_SPLIT_AT / 8;
+            constexpr int C0s = NC * (R2 ? HEAL_SCHED_SPLIT_AT_RING : HEAL_SCHED_SPLIT_AT) / 8;
             constexpr int C0 = C0s < NC ? C0s : NC - 1;  // first chunk that splits
             bf16x8 ah[WM / 16], al[WM / 16], bh[2], bl[2];
             auto read_b = [&](int c, int slot) {
@@ -384,7 +420,10 @@ gemm_bf16x3_kernel(GemmArgs p)
                     acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bh[sl], al[i], acc[j][i], 0, 0, 0);
 #pragma unroll
                 for (int u = 0; u < NU; ++u)
-                    if (C0 + (u * (NC - C0)) / NU == c) store_unit(nxt, u);
+                    if (C0 + (u * (NC - C0)) / NU == c) {
+                        store_unit(nxt, u, R2 ? set : 0);
+                        if (R2) reload_unit(u, set, k_next);
+                    }
                 __builtin_amdgcn_sched_barrier(0);
             }
         };
@@ -421,33 +460,53 @@ gemm_bf16x3_kernel(GemmArgs p)
         };
 
         // Main loop, one barrier per stage: while the MFMAs consume stage kt
-        // from one LDS buffer, the loads of stage kt+1 are in flight and are
-        // then split into the other buffer.
+        // from one LDS buffer, stage kt+1 is split into the other.  Its loads
+        // were issued at the start of stage kt (one register set), or during
+        // stage kt-2 (the ring: set 1 holds stage kt+1 and set 0 stage kt+2
+        // at the top of each trip; each set is reloaded three stages ahead,
+        // clamped to the last full stage, as soon as it is split).
+        const int64_t nk_full = K / BK;  // stages without a K tail
+        const bool ring = RING && VEC && interior && nk_full >= HEAL_RING_MIN_STAGES;
+        using one_set = std::integral_constant<bool, false>;
+        using two_sets = std::integral_constant<bool, RING>;
         int64_t kt = 0;
         if (nk > 0) {
-            if (VEC && interior && BK <= K) load_stage_fast(0);
-            else load_stage_checked(0);
-            store_stage(smem0);
+            if (VEC && interior && BK <= K) {
+                load_stage_fast(0, 0);
+                if (ring) load_stage_fast(BK, RS - 1);
+            } else {
+                load_stage_checked(0);
+            }
+            store_stage(smem0, 0);
+            if (ring) load_stage_fast(2 * BK, 0);
             __syncthreads();
         }
         if (VEC && interior) {
             // two stages per trip so that each buffer is a compile-time choice
-            const int64_t nk_full = K / BK;  // stages without a K tail
+            const int64_t last = (nk_full - 1) * BK;
             for (; kt + 2 < nk_full; kt += 2) {
+                if (RING && ring) {
+                    const int64_t k3 = (kt + 3) * BK, k4 = (kt + 4) * BK;
+                    stage_fast(smem0, smem1, RS - 1, k3 < last ? k3 : last, two_sets{});
+                    __syncthreads();
+                    stage_fast(smem1, smem0, 0, k4 < last ? k4 : last, two_sets{});
+                    __syncthreads();
+                    continue;
+                }
                 if (T::CWAVES * 64 == NT) {
-                    stage_fast(smem0, smem1, (kt + 1) * BK);
+                    stage_fast(smem0, smem1, 0, (kt + 1) * BK, one_set{});
                 } else {
-                    load_stage_fast((kt + 1) * BK);
+                    load_stage_fast((kt + 1) * BK, 0);
                     if (computes) compute_stage(smem0);
-                    store_stage(smem1);
+                    store_stage(smem1, 0);
                 }
                 __syncthreads();
                 if (T::CWAVES * 64 == NT) {
-                    stage_fast(smem1, smem0, (kt + 2) * BK);
+                    stage_fast(smem1, smem0, 0, (kt + 2) * BK, one_set{});
                 } else {
-                    load_stage_fast((kt + 2) * BK);
+                    load_stage_fast((kt + 2) * BK, 0);
                     if (computes) compute_stage(smem1);
-                    store_stage(smem0);
+                    store_stage(smem0, 0);
                 }
                 __syncthreads();
             }
@@ -457,7 +516,7 @@ gemm_bf16x3_kernel(GemmArgs p)
             char *nxt = (kt & 1) ? smem0 : smem1;
             if (kt + 1 < nk) load_stage_checked((kt + 1) * BK);
             if (computes) compute_stage(cur);
-            if (kt + 1 < nk) store_stage(nxt);
+            if (kt + 1 < nk) store_stage(nxt, 0);
             __syncthreads();
         }
 
@@ -489,22 +548,22 @@ gemm_bf16x3_kernel(GemmArgs p)
     }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int NT, bool TRANS_B, bool ALPHA>
+template <int BM, int BN, int BK, int WM, int WN, int NT, int RS, bool TRANS_B, bool ALPHA>
 hipError_t launch_tile3(const GemmArgs &a, dim3 grid, hipStream_t stream)
 {
     // The 16-byte path needs every A row and every op(B) row 16-byte aligned
     // and whole quads along K (A, B stored N x K) or N (B stored K x N).
     const bool vec = a.vecA && a.vecB && a.K % 4 == 0 && (TRANS_B || a.N % 4 == 0);
     if (vec)
-        hipLaunchKernelGGL((gemm_bf16x3_kernel<BM, BN, BK, WM, WN, NT, TRANS_B, ALPHA, true>), grid,
+        hipLaunchKernelGGL((gemm_bf16x3_kernel<BM, BN, BK, WM, WN, NT, RS, TRANS_B, ALPHA, true>), grid,
                            dim3(NT), 0, stream, a);
     else
-        hipLaunchKernelGGL((gemm_bf16x3_kernel<BM, BN, BK, WM, WN, NT, TRANS_B, ALPHA, false>), grid,
+        hipLaunchKernelGGL((gemm_bf16x3_kernel<BM, BN, BK, WM, WN, NT, RS, TRANS_B, ALPHA, false>), grid,
                            dim3(NT), 0, stream, a);
     return hipGetLastError();
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int NT>
+template <int BM, int BN, int BK, int WM, int WN, int NT, int RS = 1>
 hipError_t launch_tile(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
 {
     const int64_t tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
@@ -515,10 +574,10 @@ hipError_t launch_tile(const GemmArgs &a, bool trans_b, bool use_alpha, hipStrea
     const unsigned gy = (unsigned)(gy64 < 65535 ? gy64 : 65535);
     const dim3 grid((unsigned)tiles, gy);
     if (trans_b)
-        return use_alpha ? launch_tile3<BM, BN, BK, WM, WN, NT, true, true>(a, grid, stream)
-                         : launch_tile3<BM, BN, BK, WM, WN, NT, true, false>(a, grid, stream);
-    return use_alpha ? launch_tile3<BM, BN, BK, WM, WN, NT, false, true>(a, grid, stream)
-                     : launch_tile3<BM, BN, BK, WM, WN, NT, false, false>(a, grid, stream);
+        return use_alpha ? launch_tile3<BM, BN, BK, WM, WN, NT, RS, true, true>(a, grid, stream)
+                         : launch_tile3<BM, BN, BK, WM, WN, NT, RS, true, false>(a, grid, stream);
+    return use_alpha ? launch_tile3<BM, BN, BK, WM, WN, NT, RS, false, true>(a, grid, stream)
+                     : launch_tile3<BM, BN, BK, WM, WN, NT, RS, false, false>(a, grid, stream);
 }
 
 }  // namespace

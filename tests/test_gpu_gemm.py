@@ -392,3 +392,25 @@ def test_entry_points_bitwise_equal():
     torch.cuda.synchronize()
     assert torch.equal(C3[0].view(torch.int32), C0.view(torch.int32))
     assert torch.equal(C3[1].view(torch.int32), C0.flip(0).view(torch.int32))
+
+
+@pytest.mark.parametrize("M,N,K", [(384, 256, 1000), (256, 384, 512), (300, 260, 640), (256, 256, 4096)],
+                         ids=["ring-ktail", "ring-8-stages", "ring-edge-tiles", "ring-deep"])
+@pytest.mark.parametrize("trans_b", [False, True], ids=["b", "bt"])
+def test_medium_register_ring(orc, M, N, K, trans_b):
+    """The medium tiles' register ring (loads two stages ahead, for at least
+    8 full 64-deep stages): interior tiles with and without a K tail after
+    the ring, edge tiles beside interior ones, both B layouts and alpha.
+    Whole output against the oracle and bitwise against the large instance."""
+    A = wl.random_matrix((M, K), seed=M + K)
+    B = wl.random_matrix((N, K) if trans_b else (K, N), seed=N + 2 * K)
+    alpha = 0.625
+    Ad, Bd = to_dev(A)[None], to_dev(B)[None]
+    announce("medium ring %dx%dx%d trans_b=%d" % (M, N, K, trans_b))
+    C = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Bd, alpha=alpha, trans_b=trans_b)
+    Cl = heal.heal_gemm_f32_instance(heal.INSTANCE_LARGE, Ad, Bd, alpha=alpha, trans_b=trans_b)
+    torch.cuda.synchronize()
+    assert torch.equal(C.view(torch.int32), Cl.view(torch.int32)), "medium differs from large"
+    Bn = np.ascontiguousarray(B.T) if trans_b else B
+    _, S = orc.gemm3(A, Bn)
+    check_tolerance(C[0].cpu().numpy(), alpha * S, alpha * abs_product(A, Bn), "medium ring")
