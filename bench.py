@@ -73,7 +73,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # the kernel each instance of heal_gemm_f32 launches (16-byte aligned
 # operands), and the sources that define it
 KERNEL_NAMES = {1: "gemm_large8_kernel (256x256 tiles, 8 waves of 64x128)",
-                2: "gemm_bf16x3_kernel<128,128,64,32,64,512> (medium, 8 waves)",
+                2: "gemm_bf16x3_kernel<128,128,64,32,64,512,2> (medium, 8 waves, register ring)",
                 3: "gemm_skinny_kernel (column strips, M <= 64)"}
 KERNEL_SOURCES = {1: ["heal_gemm_large.hip", "heal_device.h", "heal_internal.h"],
                   2: ["heal_gemm.hip", "heal_device.h", "heal_internal.h"],
