@@ -62,6 +62,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, i
 //    transposed 8-byte store instruction (32 lanes per cycle) covers all
 //    banks; it permutes rows within aligned groups of 16, which fragment
 //    reads cover whole.
+//  With 64-byte rows (32-deep stages) the layout is the large kernel's:
+//  chunk swizzle (row >> 1) & 3, odd and even rows of each 8-row group
+//  swapped when bit 2 of n is set.  An earlier (row >> 2) & 3 swizzle with
+//  a 2-bit row swap read 16.4 M LDS bank-conflict cycles per lm_head
+//  dispatch (64 rows, 256-column strips) against 0 for this one, same bits.
 template <int BK>
 struct Lds {
     static constexpr int RP = 2 * BK;
@@ -69,11 +74,11 @@ struct Lds {
     static __device__ __forceinline__ int swz(int row)
     {
         return RP >= 256 ? ((row & 15) ^ ((row >> 3) & 2)) : RP == 128 ? ((row >> 1) & 7)
-                                                                         : ((row >> 2) & 3);
+                                                                         : ((row >> 1) & 3);
     }
     static __device__ __forceinline__ int brow(int n)
     {
-        return RP >= 256 ? n : RP == 128 ? (n ^ ((n >> 2) & 1)) : (n ^ ((n >> 2) & 3));
+        return RP >= 256 ? n : (n ^ ((n >> 2) & 1));
     }
     static __device__ __forceinline__ int chunk_off(int row, int c)
     {
