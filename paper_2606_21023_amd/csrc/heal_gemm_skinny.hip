@@ -56,8 +56,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const float *base, i
 //  * chunk swizzle: the 16-byte chunk c of row r is stored at c ^ swz(r),
 //    so the 16 lanes of a fragment read (16 rows, one chunk) hit 16
 //    different 16-byte bank slots; with rows of 256 bytes or more, odd
-//    16-row groups also flip bit 1, which keeps the row-contiguous B map
-//    of 32-column strips (below) free of store conflicts;
+//    16-row groups also flip bit 1 (for the row-contiguous B map of
+//    32-column strips, below).  The hardware counters still read some
+//    conflict cycles with rows of 256 bytes or more (0.56 M per 16 x 4096 x
+//    4096 dispatch, 1.08 M at 8192 columns); a swizzle that removes them
+//    for 16-column strips left the time unchanged (22.3 vs 22.4 us): these
+//    strips are bound by their B stream, not by the LDS;
 //  * brow: the LDS row of B column n (B stored K x N), chosen so that one
 //    transposed 8-byte store instruction (32 lanes per cycle) covers all
 //    banks; it permutes rows within aligned groups of 16, which fragment
