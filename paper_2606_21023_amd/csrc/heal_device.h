@@ -79,4 +79,28 @@ __device__ __forceinline__ void unpack2_i16(int q0, int q1, uint32_t &hi, uint32
     lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, f16x2));
 }
 
+// Two 16 x 16 FP32 MFMA results of adjacent 16-column blocks, r0 and r1
+// (lane fr + 16 fg holds row fr, columns 4 fg .. 4 fg + 3 of its block),
+// rearranged for stores of whole 128-byte lines: lane (fr, fg) of x holds
+// row fr & 7, and of y row 8 + (fr & 7), columns 16 (fr >> 3) + 4 fg .. + 3
+// of the 32-column pair.  Lanes 8..15 of each 16-lane row trade halves
+// with lanes 0..7 (a DPP rotation by 8 within the row), so one store of x
+// or y writes 8 rows x 128 bytes instead of 16 rows x 64 bytes.
+__device__ __forceinline__ void whole_lines(f32x4 r0, f32x4 r1, int fr, f32x4 &x, f32x4 &y)
+{
+    const bool low = fr < 8;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        // each element through a scalar first: __builtin_bit_cast of a
+        // vector element expression compiles to element 0 for every e
+        const float a = r0[e], b = r1[e];
+        const float s0 = __builtin_bit_cast(
+            float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x128, 0xf, 0xf, false));
+        const float s1 = __builtin_bit_cast(
+            float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, b), 0x128, 0xf, 0xf, false));
+        x[e] = low ? a : s1;
+        y[e] = low ? s0 : b;
+    }
+}
+
 }  // namespace heal

@@ -57,6 +57,13 @@ constexpr int kChunk = 32;  // K depth of one bf16 MFMA: the unit of the reducti
 #ifndef HEAL_RING_MIN_STAGES
 #define HEAL_RING_MIN_STAGES 8
 #endif
+// Epilogue: pairs of 16-column blocks of a wave stored as whole 128-byte
+// lines, non-temporal.  Off: in the medium tile it costs two spilled VGPRs
+// (1024 x 1024 x 4096 4% slower; 2048 x 2048 x 256 10% faster, 2048 x 1792
+// x 4096 unchanged).
+#ifndef HEAL_TILE_C_LINES
+#define HEAL_TILE_C_LINES 0
+#endif
 // Instance configurations: BM, BN, BK, WM, WN, threads[, register sets].
 // The medium tile stages 64-deep: two MFMA chunks per barrier and per round
 // of loads (at 4096 deep 1.30-1.34x faster than 32-deep stages on 2048 x
@@ -521,27 +528,48 @@ gemm_bf16x3_kernel(GemmArgs p)
         }
 
         // ---- epilogue: FP32 accumulators -> FP32 C, no downcast ----------
+        auto result = [&](int j, int i) {
+            f32x4 v = acc[j][i];
+            if (ALPHA) v = v * p.alpha;
+            return v;
+        };
+        auto store_c = [&](int64_t m, int64_t n, f32x4 v, bool nt) {
+            if (m < M && n < N) {
+                float *cp = C + m * p.ldc + n;
+                if (VEC && p.vecC && n + 4 <= N) {
+                    if (nt)
+                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(cp));
+                    else
+                        *reinterpret_cast<f32x4 *>(cp) = v;
+                } else {
+                    cp[0] = v.x;
+                    if (n + 1 < N) cp[1] = v.y;
+                    if (n + 2 < N) cp[2] = v.z;
+                    if (n + 3 < N) cp[3] = v.w;
+                }
+            }
+        };
         if (computes) {
+            // pairs of 16-column blocks as whole 128-byte lines, streamed
+            constexpr int NL = HEAL_TILE_C_LINES && VEC ? (WN / 16) / 2 * 2 : 0;
 #pragma unroll
-            for (int j = 0; j < WN / 16; ++j) {
+            for (int j = 0; j < NL; j += 2) {
 #pragma unroll
                 for (int i = 0; i < WM / 16; ++i) {
-                    const int64_t m = m0 + wm * WM + i * 16 + fr;
-                    const int64_t n = n0 + wn * WN + j * 16 + 4 * fg;
-                    f32x4 v = acc[j][i];
-                    if (ALPHA) v = v * p.alpha;
-                    if (m < M && n < N) {
-                        float *cp = C + m * p.ldc + n;
-                        if (VEC && p.vecC && n + 4 <= N) {
-                            *reinterpret_cast<f32x4 *>(cp) = v;
-                        } else {
-                            cp[0] = v.x;
-                            if (n + 1 < N) cp[1] = v.y;
-                            if (n + 2 < N) cp[2] = v.z;
-                            if (n + 3 < N) cp[3] = v.w;
-                        }
-                    }
+                    f32x4 x, y;
+                    whole_lines(result(j, i), result(j + 1, i), fr, x, y);
+                    const int64_t mx = m0 + wm * WM + i * 16 + (fr & 7);
+                    const int64_t n = n0 + wn * WN + j * 16 + 16 * (fr >> 3) + 4 * fg;
+                    store_c(mx, n, x, true);
+                    store_c(mx + 8, n, y, true);
                 }
+            }
+#pragma unroll
+            for (int j = NL; j < WN / 16; ++j) {
+#pragma unroll
+                for (int i = 0; i < WM / 16; ++i)
+                    store_c(m0 + wm * WM + i * 16 + fr, n0 + wn * WN + j * 16 + 4 * fg, result(j, i),
+                            false);
             }
         }
         if (b + gridDim.y < p.batch) __syncthreads();  // LDS reuse by the next batch entry

@@ -75,6 +75,12 @@ constexpr uint32_t kOOB = 0x80000000u;  // buffer offset beyond every range: rea
 #ifndef HEAL_L8_VMEM_FIRST
 #define HEAL_L8_VMEM_FIRST 1
 #endif
+// Epilogue of the 8-wave form: whole-line non-temporal C stores (8192^3
+// 1.0% faster in six interleaved rounds, 2048 x 14336 x 4096 unchanged;
+// same bits).
+#ifndef HEAL_LARGE_C_LINES
+#define HEAL_LARGE_C_LINES 1
+#endif
 // 4-wave form: VALU slots of one 24-MFMA group, and VALU per slot.
 #ifndef HEAL_LARGE_VALU_SLOTS
 #define HEAL_LARGE_VALU_SLOTS 12
@@ -594,6 +600,30 @@ gemm_large8_kernel(GemmArgs p)
             __syncthreads();
         }
 
+#if HEAL_LARGE_C_LINES
+        // whole 128-byte lines per store (two adjacent 16-column blocks),
+        // non-temporal: C is written once and would only evict A and B
+        // from L2
+#pragma unroll
+        for (int j = 0; j < 8; j += 2) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                f32x4 r0 = acc[j][i], r1 = acc[j + 1][i];
+                if (ALPHA) {
+                    r0 = r0 * p.alpha;
+                    r1 = r1 * p.alpha;
+                }
+                f32x4 x, y;
+                whole_lines(r0, r1, fr, x, y);
+                const int64_t mx = m0 + wm * 64 + i * 16 + (fr & 7), my = mx + 8;
+                const int64_t n = n0 + wn * kWT + j * 16 + 16 * (fr >> 3) + 4 * fg;
+                if (mx < M && n < N)
+                    __builtin_nontemporal_store(x, reinterpret_cast<f32x4 *>(C + mx * p.ldc + n));
+                if (my < M && n < N)
+                    __builtin_nontemporal_store(y, reinterpret_cast<f32x4 *>(C + my * p.ldc + n));
+            }
+        }
+#else
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
 #pragma unroll
@@ -605,6 +635,7 @@ gemm_large8_kernel(GemmArgs p)
                 if (m < M && n < N) *reinterpret_cast<f32x4 *>(C + m * p.ldc + n) = v;
             }
         }
+#endif
     }
 }
 

@@ -52,6 +52,18 @@
 
 #include <atomic>
 
+// C stores of whole 128-byte lines (pairs of 16-column result blocks, see
+// whole_lines), against 64-byte pieces, same bits: in the hand-scheduled
+// large kernel 8192^3 0.8-2.0% and 2048 x 14336 x 4096 3-6% faster for the
+// three packed-weight products; in the generic tiles (medium and skinny)
+// 2048 x 1792 x 4096 and lm_head 2-6% faster.
+#ifndef HEAL_OP8_C_LINES
+#define HEAL_OP8_C_LINES 1
+#endif
+#ifndef HEAL_OP_C_LINES
+#define HEAL_OP_C_LINES 1
+#endif
+
 namespace heal {
 
 namespace {
@@ -482,36 +494,55 @@ gemm_op_kernel(OpArgs p)
             factor = (float)((double)p.alpha * (double)*p.maxA * (double)*p.maxB /
                              (32767.0 * 32767.0));
         }
+        auto result = [&](int j, int i) {
+            f32x4 v;
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-#pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                if (!computes) break;
-                const int64_t m = m0 + wm * WM + i * 16 + fr;
-                const int64_t n = n0 + wn * WN + j * 16 + 4 * fg;
-                f32x4 v;
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    if constexpr (OP == OP_BASE || OP == OP_FULL)
-                        v[t] = ldexpf(acc[j][i][t], -p.e);
-                    else if constexpr (OP == OP_SCORES)
-                        v[t] = acc[j][i][t] * factor;
-                    else
-                        v[t] = acc[j][i][t];
+            for (int t = 0; t < 4; ++t) {
+                if constexpr (OP == OP_BASE || OP == OP_FULL)
+                    v[t] = ldexpf(acc[j][i][t], -p.e);
+                else if constexpr (OP == OP_SCORES)
+                    v[t] = acc[j][i][t] * factor;
+                else
+                    v[t] = acc[j][i][t];
+            }
+            return v;
+        };
+        auto store_c = [&](int64_t m, int64_t n, f32x4 v) {
+            if (m < M && n < N) {
+                float *cp = C + m * p.ldc + n;
+                if (p.vecC && n + 4 <= N) {
+                    // streaming store: C is not read again here (INT16
+                    // scores 1.07x, lm_head 1.01-1.035x, others unchanged)
+                    __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(cp));
+                } else {
+                    cp[0] = v.x;
+                    if (n + 1 < N) cp[1] = v.y;
+                    if (n + 2 < N) cp[2] = v.z;
+                    if (n + 3 < N) cp[3] = v.w;
                 }
-                if (m < M && n < N) {
-                    float *cp = C + m * p.ldc + n;
-                    if (p.vecC && n + 4 <= N) {
-                        // streaming store: C is not read again here (INT16
-                        // scores 1.07x, lm_head 1.01-1.035x, others unchanged)
-                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(cp));
-                    } else {
-                        cp[0] = v.x;
-                        if (n + 1 < N) cp[1] = v.y;
-                        if (n + 2 < N) cp[2] = v.z;
-                        if (n + 3 < N) cp[3] = v.w;
-                    }
+            }
+        };
+        if (computes) {
+            // pairs of 16-column blocks as whole 128-byte lines (not in the
+            // 256-row tiles, which would spill more registers for it)
+            constexpr int FL = HEAL_OP_C_LINES && BM < 256 ? FN / 2 * 2 : 0;
+#pragma unroll
+            for (int j = 0; j < FL; j += 2) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    f32x4 x, y;
+                    whole_lines(result(j, i), result(j + 1, i), fr, x, y);
+                    const int64_t mx = m0 + wm * WM + i * 16 + (fr & 7);
+                    const int64_t n = n0 + wn * WN + j * 16 + 16 * (fr >> 3) + 4 * fg;
+                    store_c(mx, n, x);
+                    store_c(mx + 8, n, y);
                 }
+            }
+#pragma unroll
+            for (int j = FL; j < FN; ++j) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+                    store_c(m0 + wm * WM + i * 16 + fr, n0 + wn * WN + j * 16 + 4 * fg, result(j, i));
             }
         }
         if (b + gridDim.y < p.batch) __syncthreads();  // LDS reuse by the next batch entry
@@ -794,28 +825,44 @@ gemm_op8_kernel(OpArgs p)
         }
 
         // epilogue: FP32 C (2^-e acc for the FP16 forms), streaming stores
+        auto result = [&](int j, int i) {
+            f32x4 v;
 #pragma unroll
-        for (int j = 0; j < WB; ++j) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int64_t m = m0 + wm * 64 + i * 16 + fr;
-                const int64_t n = n0 + wn * (BN / 2) + j * 16 + 4 * fg;
-                f32x4 v;
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    v[t] = OP == OP_PRESPLIT ? acc[j][i][t] : ldexpf(acc[j][i][t], -p.e);
-                if (m < M && n < N) {
-                    float *cp = C + m * p.ldc + n;
-                    if (p.vecC && n + 4 <= N) {
-                        __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(cp));
-                    } else {
-                        cp[0] = v.x;
-                        if (n + 1 < N) cp[1] = v.y;
-                        if (n + 2 < N) cp[2] = v.z;
-                        if (n + 3 < N) cp[3] = v.w;
-                    }
+            for (int t = 0; t < 4; ++t)
+                v[t] = OP == OP_PRESPLIT ? acc[j][i][t] : ldexpf(acc[j][i][t], -p.e);
+            return v;
+        };
+        auto store_c = [&](int64_t m, int64_t n, f32x4 v) {
+            if (m < M && n < N) {
+                float *cp = C + m * p.ldc + n;
+                if (p.vecC && n + 4 <= N) {
+                    __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(cp));
+                } else {
+                    cp[0] = v.x;
+                    if (n + 1 < N) cp[1] = v.y;
+                    if (n + 2 < N) cp[2] = v.z;
+                    if (n + 3 < N) cp[3] = v.w;
                 }
             }
+        };
+        constexpr int WL = HEAL_OP8_C_LINES ? WB / 2 * 2 : 0;   // blocks stored in whole lines
+#pragma unroll
+        for (int j = 0; j < WL; j += 2) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                f32x4 x, y;
+                whole_lines(result(j, i), result(j + 1, i), fr, x, y);
+                const int64_t mx = m0 + wm * 64 + i * 16 + (fr & 7);
+                const int64_t n = n0 + wn * (BN / 2) + j * 16 + 16 * (fr >> 3) + 4 * fg;
+                store_c(mx, n, x);
+                store_c(mx + 8, n, y);
+            }
+        }
+#pragma unroll
+        for (int j = WL; j < WB; ++j) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                store_c(m0 + wm * 64 + i * 16 + fr, n0 + wn * (BN / 2) + j * 16 + 4 * fg, result(j, i));
         }
         if (b + gridDim.y < p.batch) __syncthreads();  // LDS reuse by the next batch entry
     }

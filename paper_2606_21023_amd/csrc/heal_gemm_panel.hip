@@ -321,9 +321,8 @@ __global__ void __launch_bounds__(PNT, PBM <= 128 ? 2 : 1) gemm_panel_kernel(Pan
             if (i + 1 < PRB) read_a(i + 1, nh, nl);
 #if HEAL_PANEL_LINES
             // both 16 x 16 results of the row block, then whole 128-byte
-            // lines per store: lanes 8..15 of each 16-lane row trade their
-            // halves (a rotation by 8 within the row), so one store holds
-            // rows 0..7 of the block, 32 columns each, the other rows 8..15
+            // lines per store: one store holds rows 0..7 of the block, 32
+            // columns each, the other rows 8..15
             f32x4 r[2];
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
@@ -338,18 +337,8 @@ __global__ void __launch_bounds__(PNT, PBM <= 128 ? 2 : 1) gemm_panel_kernel(Pan
                 if (SCORES || SCALE) a = a * scale;   // FP32 C, no downcast
                 r[j] = a;
             }
-            const bool low = fr < 8;
             f32x4 x, y;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float r0 = r[0][e], r1 = r[1][e];
-                const float r0s = __builtin_bit_cast(
-                    float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, r0), 0x128, 0xf, 0xf, false));
-                const float r1s = __builtin_bit_cast(
-                    float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, r1), 0x128, 0xf, 0xf, false));
-                x[e] = low ? r0 : r1s;
-                y[e] = low ? r0s : r1;
-            }
+            whole_lines(r[0], r[1], fr, x, y);
             {
                 const int64_t mx = m0 + 16 * i + (fr & 7), my = mx + 8;
                 const int64_t n = (int64_t)s * PBN + wave * PWN + 16 * (fr >> 3) + 4 * fg;
