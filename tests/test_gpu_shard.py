@@ -72,3 +72,36 @@ def test_shard_workload_sampled(orc, name, nrows):
     _, S = orc.gemm3(A, B, rows=rows)
     nw, ew = check_tolerance(Cr, S, abs_product(A[rows], B), name)
     print("%s rows %s normwise %.3g elementwise %.3g" % (name, rows.tolist(), nw, ew))
+
+
+@pytest.mark.parametrize("name", ["lm_head", "prefill_up"])
+def test_packed_weight_column_shards_bitwise(name):
+    """The packed-weight products (HEAL-Full, HEAL-Base, pre-split B) split
+    8 ways by columns: a shard of the packed operand is the contiguous range
+    of its 16-column blocks; each shard, packed on its own from its slice of
+    the weight as a GPU holding only that slice would (with the whole
+    weight's power-of-two scale, which the shards share), equals its block
+    of the whole product bit for bit."""
+    w = wl.WORKLOADS[name]
+    A, B = wl.make_inputs(w)
+    Ad, Bd = to_dev(A), to_dev(B)
+    W = Bd.t().contiguous()                      # the N x K weight of the layer
+    e = heal.heal_f16_weight_exponent(float(W.abs().max().item()))
+    shards = 8
+    ns = w.N // shards
+    W16 = heal.heal_pack_f16_weight(W, e)
+    Bp = heal.heal_presplit_b(Bd)
+    for products in (1, 2):
+        announce("packed shards %s: HEAL f16w products=%d" % (name, products))
+        C = heal.heal_gemm_f16w(Ad, W16, w.N, e, products)
+        for s in range(shards):
+            Ws = heal.heal_pack_f16_weight(W[s * ns:(s + 1) * ns].contiguous(), e)
+            Cs = heal.heal_gemm_f16w(Ad, Ws, ns, e, products)
+            assert torch.equal(_bits(Cs), _bits(C[:, s * ns:(s + 1) * ns])), \
+                "f16w products=%d shard %d differs" % (products, s)
+    announce("packed shards %s: pre-split" % name)
+    C = heal.heal_gemm_f32_presplit(Ad, Bp, w.N)
+    for s in range(shards):
+        Bps = heal.heal_presplit_b(Bd[:, s * ns:(s + 1) * ns].contiguous())
+        Cs = heal.heal_gemm_f32_presplit(Ad, Bps, ns)
+        assert torch.equal(_bits(Cs), _bits(C[:, s * ns:(s + 1) * ns])), "pre-split shard %d differs" % s
