@@ -501,15 +501,16 @@ def profile_summary(d, out=None):
             L.append("\nMFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 "
                      "SIMDs) = %.3f; clock = GRBM_GUI_ACTIVE / 8 / trace mean = %.2f GHz.\n"
                      % (busy / (act / 8 * 1024), act / 8 / timed.mean()))
-    # further counter passes (DIR/p4, DIR/p5, ...): cache, request-size and
-    # latency counters of the measured kernel
+    # further counter passes (DIR/p4, DIR/p5, ...): cache, request-size,
+    # latency and MFMA-operation counters of the measured kernel
     extra = {}
     for sub in sorted(glob.glob(os.path.join(d, "p[4-9]"))):
         for r in rows(os.path.join(os.path.basename(sub), "*counter_collection.csv")):
             if _kernel_base_name(r["Kernel_Name"]) == kname:
                 extra.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     if extra:
-        L.append("## Cache, request-size and latency counters, mean per dispatch\n")
+        L.append("## Further counters (cache, request sizes, latency, MFMA operations), mean per "
+                 "dispatch\n")
         L.append("| counter | mean | dispatches |")
         L.append("|---|---|---|")
         for c in sorted(extra):
@@ -526,6 +527,20 @@ def profile_summary(d, out=None):
             notes.append("mean L1-to-L2 read latency TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ "
                          "= %.0f cycles" % (m["TCP_TCC_READ_REQ_LATENCY_sum"]
                                             / max(1.0, m["TCP_TCC_READ_REQ_sum"])))
+        # matrix-core work: the MOPS counters count multiply-add operations in
+        # units of 512 flops; the product does P 16-bit products of 2MNK each
+        products = {"bf16x3": (3, "BF16"), "presplit": (3, "BF16"), "f16_full": (2, "F16"),
+                    "f16_base": (1, "F16"), "i16_scores": (4, "F16")}.get(cfg["method"])
+        if products and "SQ_INSTS_VALU_MFMA_MOPS_" + products[1] in m:
+            P, T = products
+            flops = 512.0 * m["SQ_INSTS_VALU_MFMA_MOPS_" + T]
+            want = P * 2.0 * cfg["M"] * cfg["N"] * cfg["K"] * cfg.get("batch", 1)
+            r = flops / want
+            notes.append("MFMA work: SQ_INSTS_VALU_MFMA_MOPS_%s x 512 = %.4g flops per dispatch "
+                         "= %.4f x %d product%s of 2MNK (%.4g%s)"
+                         % (T, flops, r, P, "s" if P > 1 else "", want,
+                            "; the excess is the zero padding of partial tiles"
+                            if r > 1.00005 else ", exactly"))
         if notes:
             L.append("\n" + "; ".join(notes) + ".\n")
     L.append("## bench.py line of the traced run\n")

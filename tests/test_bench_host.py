@@ -88,8 +88,13 @@ def test_profile_summary_averages_the_timed_dispatches(tmp_path):
     _write_csv(os.path.join(d, "p2", "run_counter_collection.csv"), cc,
                [[1, 1, name, "WRITE_SIZE", 50.0]] +
                [[2 + i, 2 + i, "__amd_rocclr_copyBuffer", "WRITE_SIZE", 1048576.0] for i in range(3)])
+    # MFMA operations of a 32 x 32 x 64 product: 3 products x 2MNK / 512 per dispatch
+    mops = 3 * 2 * 32 * 32 * 64 / 512
+    _write_csv(os.path.join(d, "p7", "run_counter_collection.csv"), cc,
+               [[1, 1, name, "SQ_INSTS_VALU_MFMA_MOPS_BF16", mops],
+                [2, 2, name, "SQ_INSTS_VALU_MFMA_MOPS_BF16", mops]])
     line = {"warmup": W, "steps": K, "config": {"method": "bf16x3", "workload": "square8192",
-                                                "M": 8192, "N": 8192},
+                                                "M": 32, "N": 32, "K": 64},
             "roofline": {"kernel": "gemm_large8_kernel (256x256 tiles)", "avg_launch_us": 2.0,
                          "achieved": 1000.0, "peak": 2000.0, "unit": "TFLOP/s", "bound": "mfma",
                          "frac": 0.5, "per_launch": "x"}}
@@ -104,6 +109,8 @@ def test_profile_summary_averages_the_timed_dispatches(tmp_path):
     assert "timed dispatches' trace average: 0.5000" in text
     # FETCH x2 (524288 KiB per 1 GiB copy), WRITE x1: 100 KiB * 2 + 50 KiB
     assert "Traffic %.4g bytes" % (100 * 1024 * 2.0 + 50 * 1024) in text
+    assert "| SQ_INSTS_VALU_MFMA_MOPS_BF16 | %g | 2 |" % mops in text
+    assert "= 1.0000 x 3 products of 2MNK (3.932e+05, exactly)" in text
 
 
 def test_strip_width_rule_matches_the_library():
