@@ -26,7 +26,9 @@ Prints ONE JSON line:
                profiles/traffic.json only while the kernel sources are the
                ones it was measured on, else null.
   cpu_baseline the CPU oracle timed on a bounded row sample of the same product
-  comparison   MI355X native FP32 GEMM (torch.matmul, TF32 off) on the same inputs
+  comparison   MI355X native FP32 GEMM (torch.matmul, TF32 off) on the same inputs;
+               for MFMA-bound products also one plain bf16 GEMM of the same
+               shape (hipBLASLt), timed after the timed region
   bit_repro    every timed launch writes its own output buffer (up to 64 GiB of
                them); all are compared bitwise with the first timed output
   build_id     the source hash libheal.so was built from (checked at start)
@@ -312,6 +314,30 @@ def bench_split(args, w):
                 "kernel": "split_kernel<true> (8 elements per thread and step)",
                 "per_launch": "8*n bytes (4 read, 2+2 written per element) = %.4g" % alg_bytes,
                 "avg_launch_us": round(ms * 1e3, 2)}
+    # Context for an MFMA-bound product: the vendor library's rate for ONE
+    # plain bf16 GEMM of the same shape on this board (torch.matmul on bf16
+    # copies of the inputs, hipBLASLt), timed after the timed region so that
+    # it cannot change the measured launches.
+    comparison = native()
+    if roofline["bound"] == "mfma" and not batched:
+        Ab = torch.from_numpy(A).to(dev).bfloat16()
+        Bb = torch.from_numpy(B).to(dev).bfloat16()
+        for _ in range(10):
+            Ab @ Bb
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = max(20, min(100, args.steps))
+        b0.record(torch.cuda.current_stream())
+        for _ in range(reps):
+            Ab @ Bb
+        b1.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        ms_bf16 = b0.elapsed_time(b1) / reps
+        tf_bf16 = w.flops / (ms_bf16 * 1e-3) / 1e12
+        comparison.update({"torch_bf16_matmul_tflops": round(tf_bf16, 1),
+                           "torch_bf16_matmul_frac_of_peak": round(tf_bf16 / BF16_DENSE_PEAK_TFLOPS, 4),
+                           "torch_bf16_matmul_ms": round(ms_bf16, 4)})
+        del Ab, Bb
+
     cpu = None
     if not args.no_cpu:
         from oracle import oracle
@@ -429,7 +455,12 @@ def profile_summary(d, out=None):
     L.append("|---|---|---|---|---|---|")
     for r in stats[:8]:
         n = r["Name"]
-        n = "hipBLASLt FP32 GEMM (torch.matmul comparison)" if "Cijk" in n else n[:100]
+        if "Cijk" in n:
+            t = n.split("_")[3] if n.count("_") > 3 else "?"
+            n = ("hipBLASLt %s GEMM (torch.matmul comparison)"
+                 % ("FP32" if t == "S" else "bf16" if t.startswith("B") else t))
+        else:
+            n = n[:100]
         L.append("| %s | %s | %.0f | %s | %s | %.2f |" % (n, r["Calls"], float(r["AverageNs"]),
                                                         r["MinNs"], r["MaxNs"],
                                                         float(r["Percentage"])))
@@ -817,6 +848,30 @@ def main():
                      "kernel": kernel, "per_launch": per_launch,
                      "avg_launch_us": round(avg_launch_ms * 1e3, 2)})
 
+    # Context for an MFMA-bound product: the vendor library's rate for ONE
+    # plain bf16 GEMM of the same shape on this board (torch.matmul on bf16
+    # copies of the inputs, hipBLASLt), timed after the timed region so that
+    # it cannot change the measured launches.
+    comparison = native()
+    if roofline["bound"] == "mfma" and not batched:
+        Ab = torch.from_numpy(A).to(dev).bfloat16()
+        Bb = torch.from_numpy(B).to(dev).bfloat16()
+        for _ in range(10):
+            Ab @ Bb
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = max(20, min(100, args.steps))
+        b0.record(torch.cuda.current_stream())
+        for _ in range(reps):
+            Ab @ Bb
+        b1.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        ms_bf16 = b0.elapsed_time(b1) / reps
+        tf_bf16 = w.flops / (ms_bf16 * 1e-3) / 1e12
+        comparison.update({"torch_bf16_matmul_tflops": round(tf_bf16, 1),
+                           "torch_bf16_matmul_frac_of_peak": round(tf_bf16 / BF16_DENSE_PEAK_TFLOPS, 4),
+                           "torch_bf16_matmul_ms": round(ms_bf16, 4)})
+        del Ab, Bb
+
     cpu = None
     if not args.no_cpu:
         if method == "i16_scores":
@@ -859,7 +914,7 @@ def main():
         "step_stats": stats(),
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "comparison": native(),
+        "comparison": comparison,
         "build_id": heal.build_id(),
         "wall_s": round(wall, 3),
     }
