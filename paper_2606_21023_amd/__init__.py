@@ -146,7 +146,9 @@ def _require(t, name, ndim):
         raise HealError("%s must be float32, got %s" % (name, t.dtype))
     if t.dim() != ndim:
         raise HealError("%s must have %d dimensions, got %d" % (name, ndim, t.dim()))
-    if t.numel() and t.stride(-1) != 1:
+    if t.numel() and t.size(-1) > 1 and t.stride(-1) != 1:
+        # (a last dimension of one element has no stride to respect: torch
+        # may report any, e.g. for the transpose of a one-row matrix)
         raise HealError("%s must be contiguous in its last dimension" % name)
 
 
@@ -248,7 +250,9 @@ def _require_dtype(t, name, dtype, ndim=None):
         raise HealError("%s must be %s, got %s" % (name, dtype, t.dtype))
     if ndim is not None and t.dim() != ndim:
         raise HealError("%s must have %d dimensions, got %d" % (name, ndim, t.dim()))
-    if t.numel() and t.stride(-1) != 1:
+    if t.numel() and t.size(-1) > 1 and t.stride(-1) != 1:
+        # (a last dimension of one element has no stride to respect: torch
+        # may report any, e.g. for the transpose of a one-row matrix)
         raise HealError("%s must be contiguous in its last dimension" % name)
 
 
