@@ -31,8 +31,15 @@ def abs_product(A, B):
     return np.abs(A.astype(np.float64)) @ np.abs(B.astype(np.float64))
 
 
-def check_tolerance(C, S, absAB, what=""):
-    """Assert the bars; returns (normwise, max elementwise ratio)."""
+def check_tolerance(C, S, absAB, what="", normwise_min_elements=0):
+    """Assert the bars; returns (normwise, max elementwise ratio).
+
+    The normwise bar is a statement about a whole output: on a handful of
+    elements, one sum that cancels to a small value (FP32 accumulation error
+    relative to its terms, not to the result) can exceed it while every
+    element meets the elementwise bar.  Callers that draw arbitrary shapes
+    pass normwise_min_elements to apply it only to outputs at least that
+    large; the elementwise bar always applies."""
     C = np.asarray(C, np.float64)
     S = np.asarray(S, np.float64)
     err = np.abs(C - S)
@@ -42,6 +49,7 @@ def check_tolerance(C, S, absAB, what=""):
     assert np.all(C[zero] == 0), "%s: nonzero output where |A||B| = 0" % what
     ratio = np.where(zero, 0.0, err / np.where(zero, 1.0, absAB))
     worst = float(ratio.max()) if ratio.size else 0.0
-    assert normwise <= NORMWISE_BAR, "%s: normwise %.3g > %g" % (what, normwise, NORMWISE_BAR)
+    if C.size >= normwise_min_elements:
+        assert normwise <= NORMWISE_BAR, "%s: normwise %.3g > %g" % (what, normwise, NORMWISE_BAR)
     assert worst <= ELEMENTWISE_BAR, "%s: elementwise %.3g > %g" % (what, worst, ELEMENTWISE_BAR)
     return normwise, worst

@@ -5,7 +5,8 @@ Each case draws M and N (half of them 130..600, half log-uniform over
 and an A base pointer that is 4- but not always 16-byte aligned.  For
 HEAL-Base and HEAL-Full (the packed FP16 weight) every forced instance must
 give the bits of the automatic choice, leave the padding of C untouched and
-meet the oracle's bars; the product with the pre-split B must equal
+meet the oracle's bars (the normwise one on outputs of
+256 elements or more); the product with the pre-split B must equal
 heal_gemm_f32 on the same operands bit for bit, on every instance.
 """
 import numpy as np
@@ -79,7 +80,8 @@ def test_random_packed_products(orc, case):
             assert torch.equal(got.contiguous().view(torch.int32), bits), \
                 "%s p%d: instance %d differs from the automatic choice" % (what, products, inst)
         _, S = orc.gemm_f16w(A, W, e, products)
-        check_tolerance(ref.cpu().numpy(), S, absprod, "%s p%d" % (what, products))
+        check_tolerance(ref.cpu().numpy(), S, absprod, "%s p%d" % (what, products),
+                        normwise_min_elements=256)
 
     # the pre-split B (B = W^T, K x N) against heal_gemm_f32 on the same operands
     Bd = Wd.t().contiguous()

@@ -6,7 +6,8 @@ Each case draws M and N (half of them 130..600, half log-uniform over
 width, batch strides with gaps, and base pointers that are 4- but not always
 16-byte aligned.  The automatic choice and every forced instance must give
 the same bits (the reduction order is the same in all of them), leave the
-padding of C untouched, and meet the oracle's bars on every batch entry
+padding of C untouched, and meet the oracle's bars (the normwise one on outputs of
+256 elements or more) on every batch entry
 (K = 0 must write alpha * (+0), the empty sum scaled in the epilogue).
 """
 import numpy as np
@@ -99,4 +100,5 @@ def test_random_shape_all_instances(orc, case):
         Bs = np.lib.stride_tricks.as_strided(Bbuf[off + b * sB:], (rb, cb), (4 * ldb, 4))
         B = np.ascontiguousarray(Bs.T) if trans_b else np.ascontiguousarray(Bs)
         _, S = orc.gemm3(np.ascontiguousarray(A), B, alpha=alpha)
-        check_tolerance(Cb, a32 * S, abs(a32) * abs_product(A, B), "%s, entry %d" % (what, b))
+        check_tolerance(Cb, a32 * S, abs(a32) * abs_product(A, B), "%s, entry %d" % (what, b),
+                        normwise_min_elements=256)
