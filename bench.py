@@ -322,6 +322,8 @@ def bench_split(args, w):
     if roofline["bound"] == "mfma" and not batched:
         Ab = torch.from_numpy(A).to(dev).bfloat16()
         Bb = torch.from_numpy(B).to(dev).bfloat16()
+        if w.trans_b:                       # B stored N x K
+            Bb = Bb.t().contiguous()
         for _ in range(10):
             Ab @ Bb
         b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -856,6 +858,8 @@ def main():
     if roofline["bound"] == "mfma" and not batched:
         Ab = torch.from_numpy(A).to(dev).bfloat16()
         Bb = torch.from_numpy(B).to(dev).bfloat16()
+        if w.trans_b:                       # B stored N x K
+            Bb = Bb.t().contiguous()
         for _ in range(10):
             Ab @ Bb
         b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
