@@ -97,6 +97,23 @@ def skinny_strip_width(N, M):
         if -(-N // w) >= least:
             return w
     return 32 if -(-N // 32) >= 240 else 16
+
+
+def skinny_row_groups(N, M, trans_b, batch):
+    """Row groups of the bf16x3 skinny kernel (skinny_row_groups in
+    heal_gemm_skinny.hip): where the width rule gives 16-column strips, B
+    stored K x N and one batch entry run on 32-column strips with the rows in
+    G groups (1, 2 or 4, dividing M; at most 256 workgroups, at least 128);
+    0 where they do not apply."""
+    if trans_b or batch != 1 or M < 1 or skinny_strip_width(N, M) != 16:
+        return 0
+    strips = -(-N // 32)
+    g = 1
+    while g < 4 and strips * 2 * g <= 256 and M % (2 * g) == 0:
+        g *= 2
+    return g if strips * g >= 128 else 0
+
+
 # MFMA products per 32-deep chunk and output block, and bytes per operand element
 METHODS = {
     "bf16x3": {"products": 3, "a_bytes": 4, "b_bytes": 4, "dtype": "bf16x3-f32acc"},
@@ -808,7 +825,13 @@ def main():
         traffic = measured_traffic(w.name, instance)
         kernel = KERNEL_NAMES.get(instance, "?")
         if instance == 3:
-            kernel = "gemm_skinny_kernel (%d-column strips, M <= 64)" % skinny_strip_width(w.N, w.M)
+            groups = skinny_row_groups(w.N, w.M, w.trans_b, w.batch)
+            if groups:
+                kernel = ("gemm_skinny_kernel (32-column strips, the rows in %d group%s, M <= 64)"
+                          % (groups, "s" if groups > 1 else ""))
+            else:
+                kernel = ("gemm_skinny_kernel (%d-column strips, M <= 64)"
+                          % skinny_strip_width(w.N, w.M))
     else:
         traffic = measured_traffic("%s:%s" % (method, w.name), "op")
         label = OP_INSTANCE_NAMES.get(instance, "?")

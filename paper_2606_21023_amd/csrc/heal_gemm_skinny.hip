@@ -526,10 +526,34 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 #define HEAL_SKINNY_MIN_STRIPS_SMALL 480
 #endif
 
+// Row groups.  Where the width rule leaves an output with 16-column strips
+// (fewer than HEAL_SKINNY_MIN_STRIPS of 32 columns), the product with B
+// stored K x N and one batch entry runs on 32-column strips instead, its
+// rows split into G groups (1, 2 or 4, dividing M) that run as separate
+// workgroups, as many as gives at most HEAL_SKINNY_GROUP_WGS workgroups and
+// at least HEAL_SKINNY_GROUP_MIN_WGS.  Each workgroup then requests every
+// 128-byte line of its strip whole and re-reads only its group's rows of A.
+// A row's bits do not depend on the other rows, so the result is that of
+// one group.  Measured on 4096-deep products (us; 16-column strips, then
+// the groups): 2048 columns at 16 / 64 rows 21.3 / 33.1 -> 19.2 / 21.4
+// (four groups); 3072 columns 22.7 / 33.9 -> 21.8 / 27.2 (two); 4096
+// columns 22.6 / 33.7 -> 20.9 / 26.2 (two); 5120 columns 41.5 / 64.1 ->
+// 25.9 / 38.3 (one); 6144 columns 41.1 / 64.0 -> 25.7 / 37.8 (one); 7168
+// columns 41.8 / 64.5 -> 26.5 / 38.5 (one).  More groups than that (more
+// than 256 workgroups) were slower again.
+#ifndef HEAL_SKINNY_ROW_GROUPS
+#define HEAL_SKINNY_ROW_GROUPS 1
+#endif
+#ifndef HEAL_SKINNY_GROUP_WGS
+#define HEAL_SKINNY_GROUP_WGS 256
+#endif
+#ifndef HEAL_SKINNY_GROUP_MIN_WGS
+#define HEAL_SKINNY_GROUP_MIN_WGS 128
+#endif
+
 template <int MB>
-hipError_t launch_shape(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
+hipError_t launch_width(const GemmArgs &a, int w, bool trans_b, bool use_alpha, hipStream_t stream)
 {
-    const int w = skinny_strip_width(a.N, a.M);
     if (w == 32) return launch_mb<MB, HEAL_SKINNY_S32>(a, trans_b, use_alpha, stream);
     if constexpr (MB == 1) {
         if (w == 256) return launch_mb<1, HEAL_SKINNY_W1>(a, trans_b, use_alpha, stream);
@@ -578,11 +602,33 @@ bool skinny_kernel_applies(const GemmArgs &a, bool trans_b)
     return (a.N + 15) / 16 <= 0x7fffffffLL;
 }
 
+// Row groups of an output (0: none apply; see HEAL_SKINNY_ROW_GROUPS).
+static int skinny_row_groups(int64_t N, int64_t M, bool trans_b, int64_t batch)
+{
+    if (!HEAL_SKINNY_ROW_GROUPS || trans_b || batch != 1 || M < 1 || skinny_strip_width(N, M) != 16)
+        return 0;
+    const int64_t strips = (N + 31) / 32;
+    int g = 1;
+    while (g < 4 && strips * 2 * g <= HEAL_SKINNY_GROUP_WGS && M % (2 * g) == 0) g *= 2;
+    return strips * g >= HEAL_SKINNY_GROUP_MIN_WGS ? g : 0;
+}
+
 hipError_t launch_gemm_skinny(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)
 {
-    if (a.M <= 16) return launch_shape<1>(a, trans_b, use_alpha, stream);
-    if (a.M <= 32) return launch_shape<2>(a, trans_b, use_alpha, stream);
-    return launch_shape<4>(a, trans_b, use_alpha, stream);
+    GemmArgs r = a;
+    int w = skinny_strip_width(a.N, a.M);
+    if (const int g = skinny_row_groups(a.N, a.M, trans_b, a.batch)) {
+        // the groups as batch entries: rows M/g each, B shared
+        w = 32;
+        r.M = a.M / g;
+        r.batch = g;
+        r.strideA = r.M * a.lda;
+        r.strideB = 0;
+        r.strideC = r.M * a.ldc;
+    }
+    if (r.M <= 16) return launch_width<1>(r, w, trans_b, use_alpha, stream);
+    if (r.M <= 32) return launch_width<2>(r, w, trans_b, use_alpha, stream);
+    return launch_width<4>(r, w, trans_b, use_alpha, stream);
 }
 
 }  // namespace heal

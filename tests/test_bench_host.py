@@ -122,6 +122,14 @@ def test_strip_width_rule_matches_the_library():
     big = int(re.search(r"#define HEAL_SKINNY_MIN_STRIPS (\d+)", src).group(1))
     small = int(re.search(r"#define HEAL_SKINNY_MIN_STRIPS_SMALL (\d+)", src).group(1))
     assert (big, small) == (240, 480)
+    assert re.search(r"#define HEAL_SKINNY_GROUP_WGS 256\b", src)
+    assert re.search(r"#define HEAL_SKINNY_GROUP_MIN_WGS 128\b", src)
+    rg = bench.skinny_row_groups
+    # decode (4096 columns): two groups of 32-column strips for even M
+    assert [rg(4096, m, False, 1) for m in (1, 15, 16, 64)] == [1, 1, 2, 2]
+    assert [rg(2048, m, False, 1) for m in (1, 2, 4, 16)] == [0, 2, 4, 4]
+    assert [rg(6144, 16, False, 1), rg(4096, 16, True, 1), rg(4096, 16, False, 2)] == [1, 0, 0]
+    assert rg(8192, 16, False, 1) == 0            # 32-column strips by the width rule
     sw = bench.skinny_strip_width
     assert [sw(4096, m) for m in (1, 16, 17, 64)] == [16, 16, 16, 16]
     assert [sw(8192, m) for m in (16, 64)] == [32, 32]

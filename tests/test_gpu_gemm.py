@@ -292,6 +292,33 @@ def test_skinny_every_m_bitwise(N, K):
         assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "M=%d differs" % m
 
 
+# outputs the width rule leaves with 16-column strips, which run as 32-column
+# strips with their rows in 1, 2 or 4 groups (up to 256 workgroups): ragged
+# last strips, a K tail, and group counts that change with M's divisibility
+ROW_GROUP_SHAPES = [(2052, 260), (3072, 100), (4100, 36), (5120, 68), (7168, 36)]
+
+
+@pytest.mark.parametrize("N,K", ROW_GROUP_SHAPES, ids=lambda v: str(v))
+def test_skinny_row_groups_every_m(orc, N, K):
+    """Every row count 1..64 through the skinny instance where its rows run
+    in groups: each row bitwise equal to the medium instance's row of the
+    full 64-row product; 16 and 64 rows element by element against the
+    oracle."""
+    A = wl.random_matrix((64, K), seed=5 * N + K)
+    B = wl.random_matrix((K, N), seed=N + 3 * K)
+    Ad, Bd = to_dev(A), to_dev(B)
+    announce("skinny row groups every M %dx%d" % (N, K))
+    ref = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Bd)
+    torch.cuda.synchronize()
+    for m in range(1, 65):
+        C = heal.heal_gemm_f32_instance(heal.INSTANCE_SKINNY, Ad[:m], Bd)
+        torch.cuda.synchronize()
+        assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "M=%d differs" % m
+    for m in (16, 64):
+        _, S = orc.gemm3(A[:m], B)
+        check_tolerance(ref[:m].cpu().numpy(), S, abs_product(A[:m], B), "row groups M=%d" % m)
+
+
 @pytest.mark.parametrize("N,K", SKINNY_WIDTHS[2:], ids=SKINNY_WIDTH_IDS[2:])
 def test_skinny_widths_trans_b_alpha(orc, N, K):
     """The wider strips with B stored N x K and alpha, at the row counts
