@@ -101,17 +101,19 @@ def skinny_strip_width(N, M):
 
 def skinny_row_groups(N, M, trans_b, batch):
     """Row groups of the bf16x3 skinny kernel (skinny_row_groups in
-    heal_gemm_skinny.hip): where the width rule gives 16-column strips, B
-    stored K x N and one batch entry run on 32-column strips with the rows in
-    G groups (1, 2 or 4, dividing M; at most 256 workgroups, at least 128);
-    0 where they do not apply."""
-    if trans_b or batch != 1 or M < 1 or skinny_strip_width(N, M) != 16:
+    heal_gemm_skinny.hip): where the width rule gives 16-column strips, a
+    product with one batch entry runs on 32-column strips with the rows in
+    G groups (1, 2 or 4, dividing M; at most 256 workgroups, at least 128;
+    with B stored N x K more than one group only above 32 rows, and at
+    least 160 workgroups); 0 where they do not apply."""
+    if batch != 1 or M < 1 or skinny_strip_width(N, M) != 16:
         return 0
     strips = -(-N // 32)
+    gmax = 1 if trans_b and M <= 32 else 4
     g = 1
-    while g < 4 and strips * 2 * g <= 256 and M % (2 * g) == 0:
+    while g < gmax and strips * 2 * g <= 256 and M % (2 * g) == 0:
         g *= 2
-    return g if strips * g >= 128 else 0
+    return g if strips * g >= (160 if trans_b else 128) else 0
 
 
 # MFMA products per 32-deep chunk and output block, and bytes per operand element

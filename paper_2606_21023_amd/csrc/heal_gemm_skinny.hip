@@ -527,20 +527,27 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 #endif
 
 // Row groups.  Where the width rule leaves an output with 16-column strips
-// (fewer than HEAL_SKINNY_MIN_STRIPS of 32 columns), the product with B
-// stored K x N and one batch entry runs on 32-column strips instead, its
-// rows split into G groups (1, 2 or 4, dividing M) that run as separate
-// workgroups, as many as gives at most HEAL_SKINNY_GROUP_WGS workgroups and
-// at least HEAL_SKINNY_GROUP_MIN_WGS.  Each workgroup then requests every
-// 128-byte line of its strip whole and re-reads only its group's rows of A.
-// A row's bits do not depend on the other rows, so the result is that of
-// one group.  Measured on 4096-deep products (us; 16-column strips, then
-// the groups): 2048 columns at 16 / 64 rows 21.3 / 33.1 -> 19.2 / 21.4
-// (four groups); 3072 columns 22.7 / 33.9 -> 21.8 / 27.2 (two); 4096
-// columns 22.6 / 33.7 -> 20.9 / 26.2 (two); 5120 columns 41.5 / 64.1 ->
-// 25.9 / 38.3 (one); 6144 columns 41.1 / 64.0 -> 25.7 / 37.8 (one); 7168
-// columns 41.8 / 64.5 -> 26.5 / 38.5 (one).  More groups than that (more
-// than 256 workgroups) were slower again.
+// (fewer than HEAL_SKINNY_MIN_STRIPS of 32 columns), a product with one
+// batch entry runs on 32-column strips instead, its rows split into G
+// groups (1, 2 or 4, dividing M) that run as separate workgroups, as many
+// as gives at most HEAL_SKINNY_GROUP_WGS workgroups and at least
+// HEAL_SKINNY_GROUP_MIN_WGS.  With B stored K x N each workgroup then
+// requests every 128-byte line of its strip whole (a 16-column strip reads
+// half lines) and re-reads only its group's rows of A.  A row's bits do not
+// depend on the other rows, so the result is that of one group.  Measured
+// on 4096-deep products (us; 16-column strips, then the groups): 2048
+// columns at 16 / 64 rows 21.3 / 33.1 -> 19.2 / 21.4 (four groups); 3072
+// columns 22.7 / 33.9 -> 21.8 / 27.2 (two); 4096 columns 22.6 / 33.7 ->
+// 20.9 / 26.2 (two); 5120 columns 41.5 / 64.1 -> 25.9 / 38.3 (one); 6144
+// columns 41.1 / 64.0 -> 25.7 / 37.8 (one); 7168 columns 41.8 / 64.5 ->
+// 26.5 / 38.5 (one).  More groups than that (more than 256 workgroups) were
+// slower again.  With B stored N x K a 16-column strip already reads whole
+// lines, and only A's re-reads favour groups: there they apply with more
+// than 32 rows (2048 / 4096 columns at 64 rows 31.1 / 33.1 -> 17.4 / 23.2;
+// at 16 rows they were slower, 14.3 / 16.7 -> 16.5 / 17.7), and one group
+// of 32-column strips needs HEAL_SKINNY_GROUP_MIN_WGS_NK workgroups (6144
+// columns 26.1 / 60.1 -> 21.3 / 34.0; 4096 columns at 16 rows, 128
+// workgroups, 16.7 -> 18.2).
 #ifndef HEAL_SKINNY_ROW_GROUPS
 #define HEAL_SKINNY_ROW_GROUPS 1
 #endif
@@ -549,6 +556,9 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 #endif
 #ifndef HEAL_SKINNY_GROUP_MIN_WGS
 #define HEAL_SKINNY_GROUP_MIN_WGS 128
+#endif
+#ifndef HEAL_SKINNY_GROUP_MIN_WGS_NK
+#define HEAL_SKINNY_GROUP_MIN_WGS_NK 160
 #endif
 
 template <int MB>
@@ -605,12 +615,14 @@ bool skinny_kernel_applies(const GemmArgs &a, bool trans_b)
 // Row groups of an output (0: none apply; see HEAL_SKINNY_ROW_GROUPS).
 static int skinny_row_groups(int64_t N, int64_t M, bool trans_b, int64_t batch)
 {
-    if (!HEAL_SKINNY_ROW_GROUPS || trans_b || batch != 1 || M < 1 || skinny_strip_width(N, M) != 16)
+    if (!HEAL_SKINNY_ROW_GROUPS || batch != 1 || M < 1 || skinny_strip_width(N, M) != 16)
         return 0;
     const int64_t strips = (N + 31) / 32;
+    const int gmax = trans_b && M <= 32 ? 1 : 4;
     int g = 1;
-    while (g < 4 && strips * 2 * g <= HEAL_SKINNY_GROUP_WGS && M % (2 * g) == 0) g *= 2;
-    return strips * g >= HEAL_SKINNY_GROUP_MIN_WGS ? g : 0;
+    while (g < gmax && strips * 2 * g <= HEAL_SKINNY_GROUP_WGS && M % (2 * g) == 0) g *= 2;
+    const int64_t least = trans_b ? HEAL_SKINNY_GROUP_MIN_WGS_NK : HEAL_SKINNY_GROUP_MIN_WGS;
+    return strips * g >= least ? g : 0;
 }
 
 hipError_t launch_gemm_skinny(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_t stream)

@@ -129,6 +129,10 @@ def test_strip_width_rule_matches_the_library():
     assert [rg(4096, m, False, 1) for m in (1, 15, 16, 64)] == [1, 1, 2, 2]
     assert [rg(2048, m, False, 1) for m in (1, 2, 4, 16)] == [0, 2, 4, 4]
     assert [rg(6144, 16, False, 1), rg(4096, 16, True, 1), rg(4096, 16, False, 2)] == [1, 0, 0]
+    assert re.search(r"#define HEAL_SKINNY_GROUP_MIN_WGS_NK 160\b", src)
+    # B stored N x K: groups above 32 rows, one group from 160 strips
+    assert [rg(4096, 64, True, 1), rg(2048, 64, True, 1), rg(6144, 16, True, 1)] == [2, 4, 1]
+    assert [rg(4096, 32, True, 1), rg(5120, 7, True, 1)] == [0, 1]
     assert rg(8192, 16, False, 1) == 0            # 32-column strips by the width rule
     sw = bench.skinny_strip_width
     assert [sw(4096, m) for m in (1, 16, 17, 64)] == [16, 16, 16, 16]

@@ -298,20 +298,23 @@ def test_skinny_every_m_bitwise(N, K):
 ROW_GROUP_SHAPES = [(2052, 260), (3072, 100), (4100, 36), (5120, 68), (7168, 36)]
 
 
+@pytest.mark.parametrize("trans_b", [False, True], ids=["kxn", "nxk"])
 @pytest.mark.parametrize("N,K", ROW_GROUP_SHAPES, ids=lambda v: str(v))
-def test_skinny_row_groups_every_m(orc, N, K):
+def test_skinny_row_groups_every_m(orc, N, K, trans_b):
     """Every row count 1..64 through the skinny instance where its rows run
-    in groups: each row bitwise equal to the medium instance's row of the
-    full 64-row product; 16 and 64 rows element by element against the
+    in groups (B stored K x N, or N x K where more than 32 rows or enough
+    strips take them): each row bitwise equal to the medium instance's row of
+    the full 64-row product; 16 and 64 rows element by element against the
     oracle."""
     A = wl.random_matrix((64, K), seed=5 * N + K)
     B = wl.random_matrix((K, N), seed=N + 3 * K)
-    Ad, Bd = to_dev(A), to_dev(B)
-    announce("skinny row groups every M %dx%d" % (N, K))
-    ref = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Bd)
+    Ad = to_dev(A)
+    Bd = to_dev(np.ascontiguousarray(B.T)) if trans_b else to_dev(B)
+    announce("skinny row groups every M %dx%d trans_b %d" % (N, K, trans_b))
+    ref = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Bd, trans_b=trans_b)
     torch.cuda.synchronize()
     for m in range(1, 65):
-        C = heal.heal_gemm_f32_instance(heal.INSTANCE_SKINNY, Ad[:m], Bd)
+        C = heal.heal_gemm_f32_instance(heal.INSTANCE_SKINNY, Ad[:m], Bd, trans_b=trans_b)
         torch.cuda.synchronize()
         assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "M=%d differs" % m
     for m in (16, 64):
