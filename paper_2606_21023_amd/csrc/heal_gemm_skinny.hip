@@ -7,13 +7,14 @@
 // summed in FP32 and written as FP32.
 //
 // Work split.  A workgroup owns a strip of BN = 16*CB columns of C and all
-// of its (at most 64) rows, and walks K in stages of BK.  Each element of B
-// is therefore loaded and split by exactly one workgroup; A (at most 64 x K,
-// resident in L2) is re-read by every workgroup.  Strips are as wide as
-// the output allows while every CU still gets one (16 columns for 4096-wide
-// outputs, 256 for a 128256-wide lm_head): HBM bandwidth needs all CUs with
-// loads in flight, and wider strips read longer row pieces of B and fewer
-// copies of A.
+// of its (at most 64) rows, or one group of its rows, and walks K in stages
+// of BK.  Each element of B is loaded and split by the one workgroup of its
+// strip (by each row group's); A (at most 64 x K, resident in L2) is
+// re-read by every workgroup.  Strips are as wide as the output allows
+// while every CU still gets one (256 columns for a 128256-wide lm_head; 32
+// columns with the rows in two groups for a 4096-wide decode): HBM
+// bandwidth needs all CUs with loads in flight, and wider strips read
+// longer row pieces of B and fewer copies of A.
 //
 // Pipeline.  A and B are staged in a ring of R register sets: while stage s
 // is multiplied out of LDS, stage s+1 is split into the other LDS buffer and
