@@ -91,12 +91,12 @@ def skinny_strip_width(N, M):
     """Column-strip width of an M x N output with M <= 64, as the library
     picks it (skinny_strip_width in heal_gemm_skinny.hip): the widest of 256,
     128, 64 and 32 columns with at least 480 strips at up to 32 rows (240
-    above), else 32 if that still gives 240 strips, else 16."""
+    above), else 32 if that still gives 160 strips, else 16."""
     least = 480 if M <= 32 else 240
     for w in (256, 128, 64, 32):
         if -(-N // w) >= least:
             return w
-    return 32 if -(-N // 32) >= 240 else 16
+    return 32 if -(-N // 32) >= 160 else 16
 
 
 def skinny_row_groups(N, M, trans_b, batch):

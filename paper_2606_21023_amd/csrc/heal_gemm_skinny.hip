@@ -460,8 +460,14 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 // output element in one workgroup, so an output takes the widest strips of
 // which it still has enough: about one per CU at 64 rows (at least
 // HEAL_SKINNY_MIN_STRIPS), about two at 16 or 32 rows, whose A is cheaper
-// to re-read (HEAL_SKINNY_MIN_STRIPS_SMALL), but never 16-column strips
-// while 32-column ones still give one per CU.  4096 deep, 64 rows: 4096
+// to re-read (HEAL_SKINNY_MIN_STRIPS_SMALL), and 32-column strips rather
+// than 16 from HEAL_SKINNY_MIN_STRIPS_32 of them (5120 to 7168 columns at
+// 16 / 64 rows, 4096 deep: HEAL-Base 17.4-19.7 / 37.5-38.5 us with 16-column
+// strips, 16.6-18.2 / 26.5-26.9 with 32; HEAL-Full 21.4-22.2 / 53.9-54.4
+// against 18.3-18.6 / 42.5-42.8; pre-split 25.0-27.6 / 59.1-59.8 against
+// 20.9-23.5 / 46.9-47.1; bf16x3 41.1-41.8 / 64.0-64.5 against 25.7-26.5 /
+// 37.8-38.5; at 4096 columns, 128 strips of 32, the 16-column strips stay
+// faster for the packed products).  4096 deep, 64 rows: 4096
 // columns 35.4 us with 256 16-column strips (35.9 with 128 of 32 columns);
 // 8192 columns 38.7 us with 256 of 32 columns (68.0 with 512 of 16, 61.7
 // with 128 of 64); 16032 columns 66.0 us with 251 of 64 columns (127.9 with
@@ -526,9 +532,12 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 #ifndef HEAL_SKINNY_MIN_STRIPS_SMALL
 #define HEAL_SKINNY_MIN_STRIPS_SMALL 480
 #endif
+#ifndef HEAL_SKINNY_MIN_STRIPS_32
+#define HEAL_SKINNY_MIN_STRIPS_32 160
+#endif
 
 // Row groups.  Where the width rule leaves an output with 16-column strips
-// (fewer than HEAL_SKINNY_MIN_STRIPS of 32 columns), a product with one
+// (fewer than HEAL_SKINNY_MIN_STRIPS_32 of 32 columns), a product with one
 // batch entry runs on 32-column strips instead, its rows split into G
 // groups (1, 2 or 4, dividing M) that run as separate workgroups, as many
 // as gives at most HEAL_SKINNY_GROUP_WGS workgroups and at least
@@ -539,16 +548,13 @@ hipError_t launch_mb(const GemmArgs &a, bool trans_b, bool use_alpha, hipStream_
 // on 4096-deep products (us; 16-column strips, then the groups): 2048
 // columns at 16 / 64 rows 21.3 / 33.1 -> 19.2 / 21.4 (four groups); 3072
 // columns 22.7 / 33.9 -> 21.8 / 27.2 (two); 4096 columns 22.6 / 33.7 ->
-// 20.9 / 26.2 (two); 5120 columns 41.5 / 64.1 -> 25.9 / 38.3 (one); 6144
-// columns 41.1 / 64.0 -> 25.7 / 37.8 (one); 7168 columns 41.8 / 64.5 ->
-// 26.5 / 38.5 (one).  More groups than that (more than 256 workgroups) were
-// slower again.  With B stored N x K a 16-column strip already reads whole
-// lines, and only A's re-reads favour groups: there they apply with more
-// than 32 rows (2048 / 4096 columns at 64 rows 31.1 / 33.1 -> 17.4 / 23.2;
-// at 16 rows they were slower, 14.3 / 16.7 -> 16.5 / 17.7), and one group
-// of 32-column strips needs HEAL_SKINNY_GROUP_MIN_WGS_NK workgroups (6144
-// columns 26.1 / 60.1 -> 21.3 / 34.0; 4096 columns at 16 rows, 128
-// workgroups, 16.7 -> 18.2).
+// 20.9 / 26.2 (two).  More groups than that (more than 256 workgroups)
+// were slower again.  With B stored N x K a 16-column strip already reads
+// whole lines, and only A's re-reads favour groups: there they apply with
+// more than 32 rows and at least HEAL_SKINNY_GROUP_MIN_WGS_NK workgroups
+// (2048 / 4096 columns at 64 rows 31.1 / 33.1 -> 17.4 / 23.2; at 16 rows
+// they were slower, 14.3 / 16.7 -> 16.5 / 17.7; one group of 32-column
+// strips at 4096 columns, 128 workgroups, 16.7 -> 18.2).
 #ifndef HEAL_SKINNY_ROW_GROUPS
 #define HEAL_SKINNY_ROW_GROUPS 1
 #endif
@@ -589,13 +595,13 @@ hipError_t launch_width(const GemmArgs &a, int w, bool trans_b, bool use_alpha, 
 // Strip width in columns for an output of N columns and M <= 64 rows: the
 // widest of 256, 128, 64 and 32 with at least HEAL_SKINNY_MIN_STRIPS_SMALL
 // strips at up to 32 rows (HEAL_SKINNY_MIN_STRIPS above), else 32 if that
-// still gives HEAL_SKINNY_MIN_STRIPS, else 16.
+// still gives HEAL_SKINNY_MIN_STRIPS_32, else 16.
 int skinny_strip_width(int64_t N, int64_t M)
 {
     const int64_t least = M <= 32 ? HEAL_SKINNY_MIN_STRIPS_SMALL : HEAL_SKINNY_MIN_STRIPS;
     for (int w = 256; w >= 32; w /= 2)
         if ((N + w - 1) / w >= least) return w;
-    return (N + 31) / 32 >= HEAL_SKINNY_MIN_STRIPS ? 32 : 16;
+    return (N + 31) / 32 >= HEAL_SKINNY_MIN_STRIPS_32 ? 32 : 16;
 }
 
 bool skinny_kernel_applies(const GemmArgs &a, bool trans_b)

@@ -121,22 +121,24 @@ def test_strip_width_rule_matches_the_library():
         src = f.read()
     big = int(re.search(r"#define HEAL_SKINNY_MIN_STRIPS (\d+)", src).group(1))
     small = int(re.search(r"#define HEAL_SKINNY_MIN_STRIPS_SMALL (\d+)", src).group(1))
-    assert (big, small) == (240, 480)
+    s32 = int(re.search(r"#define HEAL_SKINNY_MIN_STRIPS_32 (\d+)", src).group(1))
+    assert (big, small, s32) == (240, 480, 160)
     assert re.search(r"#define HEAL_SKINNY_GROUP_WGS 256\b", src)
     assert re.search(r"#define HEAL_SKINNY_GROUP_MIN_WGS 128\b", src)
     rg = bench.skinny_row_groups
     # decode (4096 columns): two groups of 32-column strips for even M
     assert [rg(4096, m, False, 1) for m in (1, 15, 16, 64)] == [1, 1, 2, 2]
     assert [rg(2048, m, False, 1) for m in (1, 2, 4, 16)] == [0, 2, 4, 4]
-    assert [rg(6144, 16, False, 1), rg(4096, 16, True, 1), rg(4096, 16, False, 2)] == [1, 0, 0]
+    assert [rg(6144, 16, False, 1), rg(4096, 16, True, 1), rg(4096, 16, False, 2)] == [0, 0, 0]
     assert re.search(r"#define HEAL_SKINNY_GROUP_MIN_WGS_NK 160\b", src)
-    # B stored N x K: groups above 32 rows, one group from 160 strips
-    assert [rg(4096, 64, True, 1), rg(2048, 64, True, 1), rg(6144, 16, True, 1)] == [2, 4, 1]
-    assert [rg(4096, 32, True, 1), rg(5120, 7, True, 1)] == [0, 1]
+    # B stored N x K: groups above 32 rows
+    assert [rg(4096, 64, True, 1), rg(2048, 64, True, 1), rg(6144, 16, True, 1)] == [2, 4, 0]
+    assert [rg(4096, 32, True, 1), rg(1024, 64, True, 1)] == [0, 0]
     assert rg(8192, 16, False, 1) == 0            # 32-column strips by the width rule
     sw = bench.skinny_strip_width
     assert [sw(4096, m) for m in (1, 16, 17, 64)] == [16, 16, 16, 16]
     assert [sw(8192, m) for m in (16, 64)] == [32, 32]
+    assert [sw(5088, 16), sw(5089, 16), sw(6144, 64), sw(7168, 1)] == [16, 32, 32, 32]
     assert [sw(16032, m) for m in (16, 32, 33, 64)] == [32, 32, 64, 64]
     assert [sw(65536, m) for m in (16, 64)] == [128, 256]
     assert [sw(122625, 16), sw(122624, 16), sw(128256, 64)] == [256, 128, 256]
