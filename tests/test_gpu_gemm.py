@@ -298,9 +298,10 @@ def test_skinny_every_m_bitwise(N, K):
 ROW_GROUP_SHAPES = [(2052, 260), (3072, 100), (4100, 36), (5120, 68), (7168, 36)]
 
 
+@pytest.mark.parametrize("alpha", [1.0, -0.75], ids=["alpha1", "alpha-0.75"])
 @pytest.mark.parametrize("trans_b", [False, True], ids=["kxn", "nxk"])
 @pytest.mark.parametrize("N,K", ROW_GROUP_SHAPES, ids=lambda v: str(v))
-def test_skinny_row_groups_every_m(orc, N, K, trans_b):
+def test_skinny_row_groups_every_m(orc, N, K, trans_b, alpha):
     """Every row count 1..64 through the skinny instance where its rows run
     in groups (B stored K x N, or N x K where more than 32 rows or enough
     strips take them): each row bitwise equal to the medium instance's row of
@@ -310,16 +311,19 @@ def test_skinny_row_groups_every_m(orc, N, K, trans_b):
     B = wl.random_matrix((K, N), seed=N + 3 * K)
     Ad = to_dev(A)
     Bd = to_dev(np.ascontiguousarray(B.T)) if trans_b else to_dev(B)
-    announce("skinny row groups every M %dx%d trans_b %d" % (N, K, trans_b))
-    ref = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Bd, trans_b=trans_b)
+    announce("skinny row groups every M %dx%d trans_b %d alpha %g" % (N, K, trans_b, alpha))
+    ref = heal.heal_gemm_f32_instance(heal.INSTANCE_MEDIUM, Ad, Bd, alpha=alpha, trans_b=trans_b)
     torch.cuda.synchronize()
     for m in range(1, 65):
-        C = heal.heal_gemm_f32_instance(heal.INSTANCE_SKINNY, Ad[:m], Bd, trans_b=trans_b)
+        C = heal.heal_gemm_f32_instance(heal.INSTANCE_SKINNY, Ad[:m], Bd, alpha=alpha,
+                                        trans_b=trans_b)
         torch.cuda.synchronize()
         assert torch.equal(C.view(torch.int32), ref[:m].view(torch.int32)), "M=%d differs" % m
+    a32 = float(np.float32(alpha))
     for m in (16, 64):
-        _, S = orc.gemm3(A[:m], B)
-        check_tolerance(ref[:m].cpu().numpy(), S, abs_product(A[:m], B), "row groups M=%d" % m)
+        _, S = orc.gemm3(A[:m], B, alpha=alpha)
+        check_tolerance(ref[:m].cpu().numpy(), a32 * S, abs(a32) * abs_product(A[:m], B),
+                        "row groups M=%d" % m)
 
 
 @pytest.mark.parametrize("N,K", SKINNY_WIDTHS[2:], ids=SKINNY_WIDTH_IDS[2:])
